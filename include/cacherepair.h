@@ -1,0 +1,213 @@
+/*
+ * cacherepair.h -- C ABI of the CacheRepair repair forward pass on MI355X.
+ *
+ * The library computes, for the stale canonical KV cache of a packed batch of
+ * retrieval requests, the repaired cache
+ *
+ *     KV_hat = KV_stale + sigma_delta * z,
+ *     z      = KVResidualHead(LN(h^B)),
+ *
+ * where h^B is the output of B Repair Blocks over the fused stale features
+ * and token embeddings (paper Section 4.1, "StaleEncoder and token fusion",
+ * "Repair Blocks and stale-feature reinjection", "KV residual output and
+ * global RoPE").  The add is done in place in the caller's cache.  Global
+ * RoPE of the repaired K is not applied: the cache stays canonical.
+ *
+ * Conventions shared by every entry point:
+ *  - Plain C: no C++ or torch types.  All sizes are element counts unless the
+ *    name ends in _bytes.
+ *  - "device" pointers are HIP device memory on the current device; "host"
+ *    pointers are read during the call and not retained.
+ *  - stream is a hipStream_t passed as void* (NULL = the null stream).  Calls
+ *    that take a stream only enqueue work on it and never synchronise;
+ *    completion is observed through the stream.
+ *  - Every validation happens before anything is enqueued: on an error return
+ *    no device memory has been touched.
+ *  - The caller owns every buffer.  The library allocates no device memory.
+ *  - Storage dtype (bf16 or fp32) is a property of the cache layout and applies
+ *    to the cache, the token embeddings, the canonical weight blob and all
+ *    intermediate activations; accumulation is always fp32.
+ *  - No exceptions cross the ABI.  Entry points are reentrant given distinct
+ *    workspaces.
+ */
+#ifndef CACHEREPAIR_H
+#define CACHEREPAIR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define CR_API __attribute__((visibility("default")))
+#else
+#define CR_API
+#endif
+
+#define CR_ABI_VERSION 1
+#define CR_MAX_NAME 48
+
+typedef int32_t cr_status;
+enum {
+    CR_OK = 0,
+    CR_ERR_NULL = -1,       /* a required pointer is NULL                          */
+    CR_ERR_DIMS = -2,       /* repairer or cache dimensions outside what is built  */
+    CR_ERR_OFFSETS = -3,    /* chunk_offsets / request_chunks malformed            */
+    CR_ERR_LAYOUT = -4,     /* cache strides overlap, are misaligned or negative   */
+    CR_ERR_WORKSPACE = -5,  /* workspace / prepared / blob buffer too small or
+                               misaligned                                          */
+    CR_ERR_DTYPE = -6,      /* unknown storage dtype                               */
+    CR_ERR_DEVICE = -7,     /* current device is not gfx950 or cannot be queried   */
+    CR_ERR_LAUNCH = -8,     /* a kernel launch failed                              */
+    CR_ERR_CAPACITY = -9    /* caller's descriptor table is too small              */
+};
+
+enum { CR_DTYPE_BF16 = 0, CR_DTYPE_F32 = 1 };
+
+/*
+ * Stale canonical cache layout (paper Section 4.1, "Chunk-cache preparation"
+ * and "Coordinate convention"): K with local RoPE removed, V native.
+ * Element (layer l, component kv in {0 = K, 1 = V}, token t, head h, dim i)
+ * lives at  base + l*stride_layer + kv*stride_kv + t*stride_token
+ *                + h*stride_head + i        (elements; the dim stride is 1).
+ * The map must be injective (strides non-overlapping for the given extents),
+ * every stride a non-negative multiple of 8 elements and the base pointer
+ * 16-byte aligned.  head_dim must be a multiple of 32 and at most 256.
+ * Coordinate j of the residual maps to (l, kv, h, i) with
+ * j = ((l*2 + kv)*n_kv_heads + h)*head_dim + i.
+ */
+typedef struct {
+    int32_t n_layers, n_kv_heads, head_dim;
+    int32_t dtype;                 /* CR_DTYPE_BF16 or CR_DTYPE_F32 */
+    int64_t stride_layer, stride_kv, stride_token, stride_head;
+} cr_kv_layout;
+
+/*
+ * Repairer dimensions (paper Section 4.1 and Table tab:repair-scales).
+ * d_model: width E of the frozen token embedding; d_seg: per-segment
+ * projection width (1..32); d_c: width of the compressed stale features s;
+ * d_b: repair width; n_heads: attention heads (d_b / n_heads must be 32 or
+ * 64); ffn_mult: MLP expansion ratio; rope_theta: base of the repair
+ * backbone's RoPE; ln_eps: LayerNorm epsilon.  d_model and d_c must be
+ * multiples of 64 and d_b a multiple of 128.
+ */
+typedef struct {
+    int32_t d_model, d_seg, d_c, d_b, n_blocks, n_heads, ffn_mult;
+    float rope_theta, ln_eps;
+} cr_dims;
+
+/* One tensor of the canonical weight blob. */
+typedef struct {
+    char name[CR_MAX_NAME];
+    int32_t dtype;                 /* CR_DTYPE_*: storage dtype, or F32 for sigma_* */
+    int32_t ndim;
+    int64_t shape[4];
+    uint64_t offset_bytes;         /* from the blob start, 256-byte aligned */
+    uint64_t nbytes;
+} cr_tensor_desc;
+
+/* ABI version (CR_ABI_VERSION). */
+CR_API int32_t cr_version(void);
+
+/* Static, never-NULL description of a status code. */
+CR_API const char* cr_status_string(cr_status status);
+
+/*
+ * Canonical weight blob layout: every repairer tensor in blob order
+ * (paper Section 4.1; matrices are W[in][out] row-major):
+ *   w_seg[S][d_h][d_seg] b_seg[S][d_seg]  w_cmp[S*d_seg][d_c] b_cmp[d_c]
+ *   ln_enc_g[d_c] ln_enc_b[d_c]  w_tok[E][d_b] b_tok[d_b]
+ *   w_fuse[d_c+d_b][d_b] b_fuse[d_b]
+ *   per block b: blk<b>.{w_inj[d_c][d_b] b_inj ln1_g ln1_b w_qkv[d_b][3d_b]
+ *                b_qkv w_o[d_b][d_b] b_o ln2_g ln2_b w_ff1[d_b][r*d_b] b_ff1
+ *                w_ff2[r*d_b][d_b] b_ff2}
+ *   ln_f_g[d_b] ln_f_b[d_b]  w_out[d_b][D_KV] b_out[D_KV]
+ *   sigma_stale[D_KV] sigma_delta[D_KV]        (always fp32)
+ * w_qkv columns are Q | K | V, each head-major (column h*d_head + i).
+ * entries: host array of max_entries descriptors (may be NULL to query only
+ * the count); n_entries and total_bytes: host outputs.
+ * Errors: CR_ERR_NULL, CR_ERR_DIMS, CR_ERR_DTYPE, CR_ERR_CAPACITY.
+ */
+CR_API cr_status cr_weights_layout(const cr_dims* dims, const cr_kv_layout* layout,
+                            cr_tensor_desc* entries, int32_t max_entries,
+                            int32_t* n_entries, uint64_t* total_bytes);
+
+/* Size of the prepared (device-optimised) weight buffer. */
+CR_API cr_status cr_prepared_bytes(const cr_dims* dims, const cr_kv_layout* layout,
+                            uint64_t* bytes);
+
+/*
+ * One-time load step: converts the canonical blob (device, as described by
+ * cr_weights_layout) into the prepared buffer (device, cr_prepared_bytes):
+ * matrices transposed to [out][in], 1/sigma_stale folded into w_seg, vectors
+ * widened to fp32.  Exact in real arithmetic; the folded w_seg is rounded
+ * once to the storage dtype.  Both buffers 256-byte aligned.
+ */
+CR_API cr_status cr_prepare_weights(const cr_dims* dims, const cr_kv_layout* layout,
+                             const void* blob, uint64_t blob_bytes,
+                             void* prepared, uint64_t prepared_bytes, void* stream);
+
+/* Device workspace needed by cr_repair for a packed batch of n_tokens tokens. */
+CR_API cr_status cr_workspace_bytes(const cr_dims* dims, const cr_kv_layout* layout,
+                             int64_t n_tokens, uint64_t* bytes);
+
+/*
+ * Chunk schedule of the block-causal mask A_ij = 1[c(j) <= c(i)] (paper
+ * Section 4.1, Repair Blocks), restricted to tokens of the same request.
+ * For every token t it writes, to the device array rows[3*N] (N =
+ * chunk_offsets[n_chunks]):
+ *   rows[t]       = lo(t): first token of t's request,
+ *   rows[N + t]   = hi(t): one past the last token of t's chunk,
+ *   rows[2N + t]  = p_t:   0-based position of t within its request,
+ * so that t attends exactly to keys j with lo(t) <= j < hi(t).
+ * chunk_offsets: host, n_chunks+1 token offsets (0 = first, non-decreasing,
+ * empty chunks allowed).  request_chunks: host, n_requests+1 chunk offsets
+ * (first 0, last n_chunks, non-decreasing), or NULL for one request.
+ * cr_repair uses the same kernel internally.
+ */
+CR_API cr_status cr_chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
+                            const int32_t* request_chunks, int32_t n_requests,
+                            int32_t* rows, void* stream);
+
+/*
+ * The repair forward pass, in place.
+ *  kv:            device, IN/OUT, stale canonical cache in `layout`; only the
+ *                 coordinates of tokens [0, N) are read and written.
+ *  chunk_offsets, n_chunks, request_chunks, n_requests: as cr_chunk_schedule;
+ *                 N = chunk_offsets[n_chunks] tokens, packed request by request.
+ *  token_embeds:  device, [N][d_model] row-major, storage dtype: the frozen
+ *                 target embeddings E_M(x_t), already gathered.
+ *  prepared:      device, output of cr_prepare_weights for the same dims and
+ *                 layout.
+ *  workspace:     device scratch of at least cr_workspace_bytes(N) bytes,
+ *                 256-byte aligned; must not alias kv, token_embeds or
+ *                 prepared.  Contents are undefined after the call.
+ * N == 0 returns CR_OK with nothing enqueued.
+ * Errors: CR_ERR_NULL, CR_ERR_DIMS, CR_ERR_OFFSETS, CR_ERR_LAYOUT,
+ * CR_ERR_WORKSPACE, CR_ERR_DTYPE, CR_ERR_DEVICE (before any enqueue);
+ * CR_ERR_LAUNCH if a launch fails (earlier launches may have run).
+ */
+CR_API cr_status cr_repair(void* kv, const cr_kv_layout* layout,
+                    const int32_t* chunk_offsets, int32_t n_chunks,
+                    const int32_t* request_chunks, int32_t n_requests,
+                    const void* token_embeds, const cr_dims* dims,
+                    const void* prepared, uint64_t prepared_bytes,
+                    void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Debug view into the workspace after a cr_repair call that has completed:
+ * name is "s" (stale features, [N][d_c]), "h" (h^B, [N][d_b]) or "lnf"
+ * (LN_f(h^B), [N][d_b]).  Returns the byte offset from the workspace start
+ * and the row stride in elements.  These buffers hold the final values of a
+ * completed call and are overwritten by the next one.
+ */
+CR_API cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layout,
+                            int64_t n_tokens, const char* name,
+                            uint64_t* offset_bytes, int64_t* row_stride);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CACHEREPAIR_H */

@@ -22,6 +22,7 @@ Pins (tests/test_oracle.py, CPU):
   rope              2-D rotation closed form; norm preservation; shift invariance
   masked_attention  pure-Python brute force over an explicit A_ij; one chunk ==
                     unmasked SDPA; length-1 chunks == causal SDPA; constant V
+  block_causal_attention  equals masked_attention under the explicit A_ij
   stale_encoder     input-scale invariance (X*a, sigma*a); zero-weight closed
                     forms
   repair            zero head returns the stale cache exactly; bias-only head
@@ -42,7 +43,8 @@ from scipy.special import erf
 
 __all__ = [
     "layer_norm", "gelu", "rope", "token_chunk_ids", "token_request_ids",
-    "positions", "block_causal_allowed", "masked_attention", "stale_encoder",
+    "positions", "block_causal_allowed", "masked_attention", "block_causal_attention",
+    "stale_encoder",
     "token_fusion", "repair_block", "repair_features", "apply_head", "repair",
 ]
 
@@ -61,7 +63,12 @@ def layer_norm(x: np.ndarray, g: np.ndarray, b: np.ndarray, eps: float) -> np.nd
 def gelu(x: np.ndarray) -> np.ndarray:
     """Exact GELU: x * Phi(x) with Phi the standard normal CDF."""
     x = np.asarray(x, F64)
-    return 0.5 * x * (1.0 + erf(x / math.sqrt(2.0)))
+    t = x / math.sqrt(2.0)
+    erf(t, out=t)          # t = erf(x / sqrt 2)
+    t += 1.0
+    t *= x
+    t *= 0.5               # 0.5 * x * (1 + erf(x / sqrt 2))
+    return t
 
 
 def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
@@ -128,13 +135,37 @@ def masked_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     q, k, v = (np.asarray(a, F64) for a in (q, k, v))
     n, nh, d = q.shape
     out = np.empty((n, nh, d), F64)
+    masked = ~np.asarray(allowed, bool)
     for h in range(nh):
-        scores = q[:, h, :] @ k[:, h, :].T / math.sqrt(d)
-        scores = np.where(allowed, scores, -np.inf)
-        scores = scores - scores.max(axis=1, keepdims=True)
-        p = np.exp(scores)
-        p = p / p.sum(axis=1, keepdims=True)
-        out[:, h, :] = p @ v[:, h, :]
+        scores = q[:, h, :] @ k[:, h, :].T
+        scores /= math.sqrt(d)
+        scores[masked] = -np.inf
+        scores -= scores.max(axis=1, keepdims=True)
+        np.exp(scores, out=scores)                    # masked entries become exactly 0
+        scores /= scores.sum(axis=1, keepdims=True)   # softmax over the allowed keys
+        out[:, h, :] = scores @ v[:, h, :]
+    return out
+
+
+def block_causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                           chunk_offsets: np.ndarray, request_chunks: np.ndarray) -> np.ndarray:
+    """Attention under A_ij = 1[c(j) <= c(i)] within each request.
+
+    For the rows of chunk c, the allowed keys are exactly the tokens from the
+    first token of c's request up to the last token of c, so each chunk's
+    rows attend, unmasked, to that contiguous key range.
+    """
+    off = np.asarray(chunk_offsets, np.int64)
+    rc = np.asarray(request_chunks, np.int64)
+    out = np.empty(np.shape(q), F64)
+    for r in range(len(rc) - 1):
+        start = off[rc[r]]
+        for c in range(rc[r], rc[r + 1]):
+            a, b = off[c], off[c + 1]
+            if a == b:
+                continue
+            everything = np.ones((b - a, b - start), bool)
+            out[a:b] = masked_attention(q[a:b], k[start:b], v[start:b], everything)
     return out
 
 
@@ -167,8 +198,8 @@ def token_fusion(s: np.ndarray, token_embeds: np.ndarray, w: Dict[str, np.ndarra
 
 
 def repair_block(h: np.ndarray, s: np.ndarray, w: Dict[str, np.ndarray], b: int,
-                 n_heads: int, allowed: np.ndarray, pos: np.ndarray,
-                 rope_theta: float, ln_eps: float) -> np.ndarray:
+                 n_heads: int, chunk_offsets: np.ndarray, request_chunks: np.ndarray,
+                 pos: np.ndarray, rope_theta: float, ln_eps: float) -> np.ndarray:
     """h^b = RepairBlock_b(h^{b-1} + P_b(s); A, p), a pre-LN Transformer block."""
     p = f"blk{b}."
     W = lambda n: np.asarray(w[p + n], F64)
@@ -182,7 +213,7 @@ def repair_block(h: np.ndarray, s: np.ndarray, w: Dict[str, np.ndarray], b: int,
     v = qkv[:, 2 * db:3 * db].reshape(N, n_heads, d)
     q = rope(q, pos, rope_theta)
     k = rope(k, pos, rope_theta)
-    o = masked_attention(q, k, v, allowed).reshape(N, db)
+    o = block_causal_attention(q, k, v, chunk_offsets, request_chunks).reshape(N, db)
     x = x + o @ W("w_o") + W("b_o")
     f = gelu(layer_norm(x, W("ln2_g"), W("ln2_b"), ln_eps) @ W("w_ff1") + W("b_ff1"))
     return x + f @ W("w_ff2") + W("b_ff2")
@@ -196,10 +227,7 @@ def repair_features(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.n
     """Everything up to LN_f(h^B): returns [N, d_b] in fp64."""
     if request_chunks is None:
         request_chunks = np.array([0, len(chunk_offsets) - 1], np.int32)
-    c = token_chunk_ids(chunk_offsets)
-    r = token_request_ids(chunk_offsets, request_chunks)
     pos = positions(chunk_offsets, request_chunks) + pos_shift
-    allowed = block_causal_allowed(c, r)
     s = stale_encoder(X, w, head_dim, ln_eps)
     h = token_fusion(s, token_embeds, w)
     if taps is not None:
@@ -207,7 +235,8 @@ def repair_features(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.n
         taps["h0"] = h
     n_blocks = sum(1 for k in w if k.endswith(".w_inj"))
     for b in range(n_blocks):
-        h = repair_block(h, s, w, b, n_heads, allowed, pos, rope_theta, ln_eps)
+        h = repair_block(h, s, w, b, n_heads, chunk_offsets, request_chunks, pos,
+                         rope_theta, ln_eps)
         if taps is not None:
             taps[f"h{b + 1}"] = h
     lnf = layer_norm(h, w["ln_f_g"], w["ln_f_b"], ln_eps)
@@ -221,8 +250,11 @@ def apply_head(X_cols: np.ndarray, lnf: np.ndarray, w: Dict[str, np.ndarray],
     """KV_hat = KV_stale + sigma_delta * (LN_f(h^B) @ W_out + b_out) on a
     column range of the cache (Section 4.1, KV residual output).  X_cols
     holds the stale values of exactly those columns."""
-    z = lnf @ np.asarray(w["w_out"][:, cols], F64) + np.asarray(w["b_out"][cols], F64)
-    return np.asarray(X_cols, F64) + np.asarray(w["sigma_delta"][cols], F64) * z
+    z = lnf @ np.asarray(w["w_out"][:, cols], F64)
+    z += np.asarray(w["b_out"][cols], F64)            # z = LN_f(h) W_out + b_out
+    z *= np.asarray(w["sigma_delta"][cols], F64)      # sigma_delta * z
+    z += np.asarray(X_cols, F64)                      # stale + sigma_delta * z
+    return z
 
 
 def repair(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.ndarray,

@@ -1,0 +1,197 @@
+"""Thin ctypes binding of the CacheRepair C ABI (``include/cacherepair.h``).
+
+Argument marshalling only: every step of the repair forward pass runs in the
+HIP library.  Functions keep the C names; pointers are passed as integers
+(device addresses, e.g. ``tensor.data_ptr()``) and streams as integers
+(``torch.cuda.Stream.cuda_stream``) or None for the null stream.  A non-OK
+status raises :class:`CrError`.  If the built library is missing, loading
+fails loudly: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char, c_char_p, c_float, c_int32, c_int64, c_uint64, c_void_p
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcacherepair.so")
+
+CR_DTYPE_BF16 = 0
+CR_DTYPE_F32 = 1
+CR_MAX_NAME = 48
+STATUS = {
+    0: "CR_OK", -1: "CR_ERR_NULL", -2: "CR_ERR_DIMS", -3: "CR_ERR_OFFSETS",
+    -4: "CR_ERR_LAYOUT", -5: "CR_ERR_WORKSPACE", -6: "CR_ERR_DTYPE",
+    -7: "CR_ERR_DEVICE", -8: "CR_ERR_LAUNCH", -9: "CR_ERR_CAPACITY",
+}
+EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_bytes",
+           "cr_prepare_weights", "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair",
+           "cr_workspace_view"]
+
+
+class CrError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({message})")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+class cr_kv_layout(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("n_kv_heads", c_int32), ("head_dim", c_int32),
+                ("dtype", c_int32), ("stride_layer", c_int64), ("stride_kv", c_int64),
+                ("stride_token", c_int64), ("stride_head", c_int64)]
+
+
+class cr_dims(ctypes.Structure):
+    _fields_ = [("d_model", c_int32), ("d_seg", c_int32), ("d_c", c_int32), ("d_b", c_int32),
+                ("n_blocks", c_int32), ("n_heads", c_int32), ("ffn_mult", c_int32),
+                ("rope_theta", c_float), ("ln_eps", c_float)]
+
+
+class cr_tensor_desc(ctypes.Structure):
+    _fields_ = [("name", c_char * CR_MAX_NAME), ("dtype", c_int32), ("ndim", c_int32),
+                ("shape", c_int64 * 4), ("offset_bytes", c_uint64), ("nbytes", c_uint64)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library {path} is not built; run __graft_entry__.build() "
+                           "(python paper_2609_35139_amd/build.py)")
+    lib = ctypes.CDLL(path)
+    lib.cr_version.restype = c_int32
+    lib.cr_status_string.restype = c_char_p
+    lib.cr_status_string.argtypes = [c_int32]
+    P = POINTER
+    lib.cr_weights_layout.argtypes = [P(cr_dims), P(cr_kv_layout), P(cr_tensor_desc), c_int32,
+                                      P(c_int32), P(c_uint64)]
+    lib.cr_prepared_bytes.argtypes = [P(cr_dims), P(cr_kv_layout), P(c_uint64)]
+    lib.cr_prepare_weights.argtypes = [P(cr_dims), P(cr_kv_layout), c_void_p, c_uint64,
+                                       c_void_p, c_uint64, c_void_p]
+    lib.cr_workspace_bytes.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, P(c_uint64)]
+    lib.cr_chunk_schedule.argtypes = [P(c_int32), c_int32, P(c_int32), c_int32, c_void_p,
+                                      c_void_p]
+    lib.cr_repair.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
+                              c_int32, c_void_p, P(cr_dims), c_void_p, c_uint64, c_void_p,
+                              c_uint64, c_void_p]
+    lib.cr_workspace_view.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, c_char_p,
+                                      P(c_uint64), P(c_int64)]
+    for name in ["cr_weights_layout", "cr_prepared_bytes", "cr_prepare_weights",
+                 "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_workspace_view"]:
+        getattr(lib, name).restype = c_int32
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise CrError(status, where, cr_status_string(status))
+
+
+def _i32(arr) -> Tuple[object, int]:
+    if arr is None:
+        return None, 0
+    a = np.ascontiguousarray(arr, dtype=np.int32)
+    return a, len(a) - 1
+
+
+# ------------------------------------------------------------------ ABI
+def cr_version() -> int:
+    return int(load().cr_version())
+
+
+def cr_status_string(status: int) -> str:
+    return load().cr_status_string(status).decode()
+
+
+def cr_weights_layout(dims: cr_dims, layout: cr_kv_layout) -> Tuple[List[dict], int]:
+    lib = load()
+    n = c_int32(0)
+    total = c_uint64(0)
+    _check(lib.cr_weights_layout(ctypes.byref(dims), ctypes.byref(layout), None, 0,
+                                 ctypes.byref(n), ctypes.byref(total)), "cr_weights_layout")
+    table = (cr_tensor_desc * n.value)()
+    _check(lib.cr_weights_layout(ctypes.byref(dims), ctypes.byref(layout), table, n.value,
+                                 ctypes.byref(n), ctypes.byref(total)), "cr_weights_layout")
+    out = []
+    for e in table:
+        out.append({"name": e.name.decode(), "dtype": e.dtype,
+                    "shape": tuple(e.shape[k] for k in range(e.ndim)),
+                    "offset_bytes": e.offset_bytes, "nbytes": e.nbytes})
+    return out, total.value
+
+
+def cr_prepared_bytes(dims: cr_dims, layout: cr_kv_layout) -> int:
+    b = c_uint64(0)
+    _check(load().cr_prepared_bytes(ctypes.byref(dims), ctypes.byref(layout), ctypes.byref(b)),
+           "cr_prepared_bytes")
+    return b.value
+
+
+def cr_prepare_weights(dims: cr_dims, layout: cr_kv_layout, blob: int, blob_bytes: int,
+                       prepared: int, prepared_bytes: int, stream: Optional[int] = None) -> None:
+    _check(load().cr_prepare_weights(ctypes.byref(dims), ctypes.byref(layout), blob, blob_bytes,
+                                     prepared, prepared_bytes, stream), "cr_prepare_weights")
+
+
+def cr_workspace_bytes(dims: cr_dims, layout: cr_kv_layout, n_tokens: int) -> int:
+    b = c_uint64(0)
+    _check(load().cr_workspace_bytes(ctypes.byref(dims), ctypes.byref(layout), n_tokens,
+                                     ctypes.byref(b)), "cr_workspace_bytes")
+    return b.value
+
+
+def cr_chunk_schedule(chunk_offsets: Sequence[int], request_chunks: Optional[Sequence[int]],
+                      rows: int, stream: Optional[int] = None) -> None:
+    off, m = _i32(chunk_offsets)
+    req, r = _i32(request_chunks)
+    _check(load().cr_chunk_schedule(
+        off.ctypes.data_as(POINTER(c_int32)), m,
+        req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r, rows, stream),
+        "cr_chunk_schedule")
+
+
+def cr_repair(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
+              request_chunks: Optional[Sequence[int]], token_embeds: int, dims: cr_dims,
+              prepared: int, prepared_bytes: int, workspace: int, workspace_bytes: int,
+              stream: Optional[int] = None) -> None:
+    off, m = _i32(chunk_offsets)
+    req, r = _i32(request_chunks)
+    _check(load().cr_repair(
+        kv, ctypes.byref(layout), off.ctypes.data_as(POINTER(c_int32)), m,
+        req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r,
+        token_embeds, ctypes.byref(dims), prepared, prepared_bytes, workspace, workspace_bytes,
+        stream), "cr_repair")
+
+
+def cr_workspace_view(dims: cr_dims, layout: cr_kv_layout, n_tokens: int,
+                      name: str) -> Tuple[int, int]:
+    off = c_uint64(0)
+    ld = c_int64(0)
+    _check(load().cr_workspace_view(ctypes.byref(dims), ctypes.byref(layout), n_tokens,
+                                    name.encode(), ctypes.byref(off), ctypes.byref(ld)),
+           "cr_workspace_view")
+    return off.value, ld.value
+
+
+# ---------------------------------------------------------- conveniences
+def make_dims(d_model, d_seg, d_c, d_b, n_blocks, n_heads, ffn_mult, rope_theta=1e4,
+              ln_eps=1e-5) -> cr_dims:
+    return cr_dims(d_model, d_seg, d_c, d_b, n_blocks, n_heads, ffn_mult, rope_theta, ln_eps)
+
+
+def layer_major_layout(n_layers, n_kv_heads, head_dim, n_tokens, dtype) -> cr_kv_layout:
+    """Strides of a contiguous [L][2][N][H][d_h] cache."""
+    sH = head_dim
+    sT = n_kv_heads * head_dim
+    sKV = n_tokens * sT
+    return cr_kv_layout(n_layers, n_kv_heads, head_dim, dtype, 2 * sKV, sKV, sT, sH)

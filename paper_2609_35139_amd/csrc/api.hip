@@ -1,0 +1,511 @@
+// C ABI of the CacheRepair repair forward pass: validation, buffer layouts
+// and the kernel sequence of one call.  See include/cacherepair.h.
+#include "../../include/cacherepair.h"
+
+#include <algorithm>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "launch.h"
+
+namespace {
+
+using cr::bf16;
+
+constexpr uint64_t ALIGN = 256;
+inline uint64_t align_up(uint64_t x, uint64_t a = ALIGN) { return (x + a - 1) / a * a; }
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+struct Arena {
+  uint64_t off = 0;
+  uint64_t take(uint64_t bytes) {
+    const uint64_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  }
+};
+
+inline size_t esize(int dtype) { return dtype == CR_DTYPE_F32 ? 4 : 2; }
+
+// ------------------------------------------------------------ validation
+cr_status check_dtype(const cr_kv_layout* l) {
+  return (l->dtype == CR_DTYPE_BF16 || l->dtype == CR_DTYPE_F32) ? CR_OK : CR_ERR_DTYPE;
+}
+
+cr_status check_dims(const cr_dims* d, const cr_kv_layout* l) {
+  if (!d || !l) return CR_ERR_NULL;
+  cr_status st = check_dtype(l);
+  if (st != CR_OK) return st;
+  if (l->n_layers < 1 || l->n_kv_heads < 1 || l->head_dim < 32 || l->head_dim > 256 ||
+      l->head_dim % 32 != 0)
+    return CR_ERR_DIMS;
+  if ((int64_t)2 * l->n_layers * l->n_kv_heads * l->head_dim > (int64_t)1 << 24) return CR_ERR_DIMS;
+  if (d->d_model < 64 || d->d_model % 64 != 0) return CR_ERR_DIMS;
+  if (d->d_seg < 1 || d->d_seg > 32) return CR_ERR_DIMS;
+  if (d->d_c < 64 || d->d_c % 64 != 0 || d->d_c > 2048) return CR_ERR_DIMS;
+  if (d->d_b < 128 || d->d_b % 128 != 0 || d->d_b > 2048) return CR_ERR_DIMS;
+  if (d->n_heads < 1 || d->d_b % d->n_heads != 0) return CR_ERR_DIMS;
+  const int dh = d->d_b / d->n_heads;
+  if (dh != 32 && dh != 64) return CR_ERR_DIMS;
+  if (d->n_blocks < 0 || d->n_blocks > 256) return CR_ERR_DIMS;
+  if (d->ffn_mult < 1 || d->ffn_mult > 16) return CR_ERR_DIMS;
+  if (!(d->rope_theta > 0.f) || !(d->ln_eps >= 0.f)) return CR_ERR_DIMS;
+  return CR_OK;
+}
+
+// Injective index map: with dims sorted by stride, each stride must exceed the
+// largest offset reachable through the dims inside it.
+cr_status check_layout(const cr_kv_layout* l, int64_t n_tokens) {
+  const int64_t st[4] = {l->stride_layer, l->stride_kv, l->stride_token, l->stride_head};
+  const int64_t ext[4] = {l->n_layers, 2, n_tokens, l->n_kv_heads};
+  struct D { int64_t s, e; };
+  std::vector<D> dims{{1, l->head_dim}};
+  for (int i = 0; i < 4; ++i) {
+    if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
+    if (ext[i] > 1) dims.push_back({st[i], ext[i]});
+  }
+  if (n_tokens == 0) return CR_OK;  // no element is addressed
+  std::sort(dims.begin(), dims.end(), [](const D& a, const D& b) { return a.s < b.s; });
+  int64_t reach = 0;  // largest offset reachable by the dims visited so far
+  for (const D& x : dims) {
+    if (x.s <= reach) return CR_ERR_LAYOUT;
+    reach += x.s * (x.e - 1);
+  }
+  return CR_OK;
+}
+
+cr_status check_offsets(const int32_t* off, int32_t n_chunks, const int32_t* req,
+                        int32_t n_req) {
+  if (!off) return CR_ERR_NULL;
+  if (n_chunks < 1) return CR_ERR_OFFSETS;
+  if (off[0] != 0) return CR_ERR_OFFSETS;
+  for (int i = 0; i < n_chunks; ++i)
+    if (off[i + 1] < off[i]) return CR_ERR_OFFSETS;
+  if (req) {
+    if (n_req < 1 || req[0] != 0 || req[n_req] != n_chunks) return CR_ERR_OFFSETS;
+    for (int i = 0; i < n_req; ++i)
+      if (req[i + 1] < req[i]) return CR_ERR_OFFSETS;
+  }
+  return CR_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+cr_status check_device() {
+  static int ok[64] = {0};  // 0 unknown, 1 gfx950, -1 not
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return CR_ERR_DEVICE;
+  if (dev < 64 && ok[dev]) return ok[dev] > 0 ? CR_OK : CR_ERR_DEVICE;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return CR_ERR_DEVICE;
+  const bool good = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev < 64) ok[dev] = good ? 1 : -1;
+  return good ? CR_OK : CR_ERR_DEVICE;
+}
+
+// ------------------------------------------------------------- layouts
+struct Tensor {
+  std::string name;
+  int dtype;
+  std::vector<int64_t> shape;
+  uint64_t off = 0, nbytes = 0;
+};
+
+// Canonical blob: every tensor of the repairer in blob order.
+std::vector<Tensor> canonical(const cr_dims* d, const cr_kv_layout* l, uint64_t* total) {
+  const int T = l->dtype;
+  const int64_t S = 2LL * l->n_layers * l->n_kv_heads, dh = l->head_dim, D = S * dh;
+  const int64_t dc = d->d_c, db = d->d_b, E = d->d_model, r = d->ffn_mult, ds = d->d_seg;
+  std::vector<Tensor> v;
+  auto add = [&](const std::string& n, int dt, std::vector<int64_t> sh) { v.push_back({n, dt, sh}); };
+  add("w_seg", T, {S, dh, ds}); add("b_seg", T, {S, ds});
+  add("w_cmp", T, {S * ds, dc}); add("b_cmp", T, {dc});
+  add("ln_enc_g", T, {dc}); add("ln_enc_b", T, {dc});
+  add("w_tok", T, {E, db}); add("b_tok", T, {db});
+  add("w_fuse", T, {dc + db, db}); add("b_fuse", T, {db});
+  for (int b = 0; b < d->n_blocks; ++b) {
+    const std::string p = "blk" + std::to_string(b) + ".";
+    add(p + "w_inj", T, {dc, db}); add(p + "b_inj", T, {db});
+    add(p + "ln1_g", T, {db}); add(p + "ln1_b", T, {db});
+    add(p + "w_qkv", T, {db, 3 * db}); add(p + "b_qkv", T, {3 * db});
+    add(p + "w_o", T, {db, db}); add(p + "b_o", T, {db});
+    add(p + "ln2_g", T, {db}); add(p + "ln2_b", T, {db});
+    add(p + "w_ff1", T, {db, r * db}); add(p + "b_ff1", T, {r * db});
+    add(p + "w_ff2", T, {r * db, db}); add(p + "b_ff2", T, {db});
+  }
+  add("ln_f_g", T, {db}); add("ln_f_b", T, {db});
+  add("w_out", T, {db, D}); add("b_out", T, {D});
+  add("sigma_stale", CR_DTYPE_F32, {D}); add("sigma_delta", CR_DTYPE_F32, {D});
+  Arena a;
+  for (Tensor& t : v) {
+    uint64_t n = 1;
+    for (int64_t s : t.shape) n *= (uint64_t)s;
+    t.nbytes = n * esize(t.dtype);
+    t.off = a.take(t.nbytes);
+  }
+  *total = a.off;
+  return v;
+}
+
+struct BlockP {
+  uint64_t w_inj, b_inj, ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_ff1, b_ff1, w_ff2,
+      b_ff2;
+};
+// Prepared (device-optimised) weights: matrices [out][in] in the storage
+// dtype, vectors fp32.
+struct Prepared {
+  int64_t kc, kc_pad;
+  uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_tok, b_tok, w_fuse, b_fuse;
+  std::vector<BlockP> blk;
+  uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta, total;
+};
+
+Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
+  const size_t T = esize(l->dtype), F = 4;
+  const int64_t S = 2LL * l->n_layers * l->n_kv_heads, dh = l->head_dim, D = S * dh;
+  const int64_t dc = d->d_c, db = d->d_b, E = d->d_model, r = d->ffn_mult;
+  Prepared p;
+  p.kc = S * d->d_seg;
+  p.kc_pad = round_up(p.kc, 64);
+  Arena a;
+  p.w_seg = a.take(S * 32 * dh * T);
+  p.b_seg = a.take(S * 32 * F);
+  p.w_cmp = a.take(dc * p.kc_pad * T);
+  p.b_cmp = a.take(dc * F); p.ln_enc_g = a.take(dc * F); p.ln_enc_b = a.take(dc * F);
+  p.w_tok = a.take(db * E * T); p.b_tok = a.take(db * F);
+  p.w_fuse = a.take(db * (dc + db) * T); p.b_fuse = a.take(db * F);
+  for (int b = 0; b < d->n_blocks; ++b) {
+    BlockP q;
+    q.w_inj = a.take(db * dc * T); q.b_inj = a.take(db * F);
+    q.ln1_g = a.take(db * F); q.ln1_b = a.take(db * F);
+    q.w_qkv = a.take(3 * db * db * T); q.b_qkv = a.take(3 * db * F);
+    q.w_o = a.take(db * db * T); q.b_o = a.take(db * F);
+    q.ln2_g = a.take(db * F); q.ln2_b = a.take(db * F);
+    q.w_ff1 = a.take(r * db * db * T); q.b_ff1 = a.take(r * db * F);
+    q.w_ff2 = a.take(db * r * db * T); q.b_ff2 = a.take(db * F);
+    p.blk.push_back(q);
+  }
+  p.ln_f_g = a.take(db * F); p.ln_f_b = a.take(db * F);
+  p.w_out = a.take(D * db * T); p.b_out = a.take(D * F); p.sigma_delta = a.take(D * F);
+  p.total = a.off;
+  return p;
+}
+
+struct Workspace {
+  int64_t n, n_pad, ldst;
+  uint64_t lo, hi, pos, rope, U, st, h, a, q, k, vt, o, f, total;
+};
+
+Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
+  const size_t T = esize(l->dtype);
+  const int64_t S = 2LL * l->n_layers * l->n_kv_heads;
+  const int64_t dc = d->d_c, db = d->d_b, r = d->ffn_mult, dhd = db / d->n_heads;
+  const int64_t kc_pad = round_up(S * d->d_seg, 64);
+  Workspace w;
+  w.n = N;
+  w.n_pad = round_up(std::max<int64_t>(N, 1), 128);
+  w.ldst = dc + db;
+  Arena a;
+  w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
+  w.rope = a.take(std::max<int64_t>(N, 1) * (dhd / 2) * 8);
+  w.U = a.take(N * kc_pad * T);
+  w.st = a.take(N * w.ldst * T);
+  w.h = a.take(N * db * T);
+  w.a = a.take(N * db * T);
+  w.q = a.take(N * db * T);
+  w.k = a.take(N * db * T);
+  w.vt = a.take(db * w.n_pad * T);
+  w.o = a.take(N * db * T);
+  w.f = a.take(N * r * db * T);
+  w.total = a.off;
+  return w;
+}
+
+#define CR_TRY(...)                                 \
+  do {                                            \
+    if ((__VA_ARGS__) != hipSuccess) return CR_ERR_LAUNCH; \
+  } while (0)
+
+template <typename T>
+cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob, char* out,
+                       hipStream_t s) {
+  uint64_t total = 0;
+  const std::vector<Tensor> c = canonical(d, l, &total);
+  const Prepared p = prepared_layout(d, l);
+  auto src = [&](const std::string& n) -> const T* {
+    for (const Tensor& t : c)
+      if (t.name == n) return reinterpret_cast<const T*>(blob + t.off);
+    return nullptr;
+  };
+  auto srcf = [&](const std::string& n) -> const float* {
+    for (const Tensor& t : c)
+      if (t.name == n) return reinterpret_cast<const float*>(blob + t.off);
+    return nullptr;
+  };
+  const int S = 2 * l->n_layers * l->n_kv_heads, dh = l->head_dim, D = S * dh;
+  const int dc = d->d_c, db = d->d_b, E = d->d_model, r = d->ffn_mult, ds = d->d_seg;
+  auto mat = [&](const std::string& n, uint64_t dst, int in, int outn, int in_pad) {
+    return cr::transpose_convert<T, T>(src(n), reinterpret_cast<T*>(out + dst), 1, in, outn, outn,
+                                       in_pad, nullptr, s);
+  };
+  auto vec = [&](const std::string& n, uint64_t dst, int len) {
+    return cr::convert_f32<T>(src(n), reinterpret_cast<float*>(out + dst), len, len, 1, 0, 0, s);
+  };
+  // 1/sigma_stale folded into the per-segment projections
+  CR_TRY(cr::transpose_convert<T, T>(src("w_seg"), reinterpret_cast<T*>(out + p.w_seg), S, dh, ds,
+                                     32, dh, srcf("sigma_stale"), s));
+  CR_TRY(cr::convert_f32<T>(src("b_seg"), reinterpret_cast<float*>(out + p.b_seg), ds, 32, S, ds,
+                            32, s));
+  CR_TRY(mat("w_cmp", p.w_cmp, (int)p.kc, dc, (int)p.kc_pad));
+  CR_TRY(vec("b_cmp", p.b_cmp, dc));
+  CR_TRY(vec("ln_enc_g", p.ln_enc_g, dc));
+  CR_TRY(vec("ln_enc_b", p.ln_enc_b, dc));
+  CR_TRY(mat("w_tok", p.w_tok, E, db, E));
+  CR_TRY(vec("b_tok", p.b_tok, db));
+  CR_TRY(mat("w_fuse", p.w_fuse, dc + db, db, dc + db));
+  CR_TRY(vec("b_fuse", p.b_fuse, db));
+  for (int b = 0; b < d->n_blocks; ++b) {
+    const std::string q = "blk" + std::to_string(b) + ".";
+    const BlockP& B = p.blk[b];
+    CR_TRY(mat(q + "w_inj", B.w_inj, dc, db, dc));
+    CR_TRY(vec(q + "b_inj", B.b_inj, db));
+    CR_TRY(vec(q + "ln1_g", B.ln1_g, db));
+    CR_TRY(vec(q + "ln1_b", B.ln1_b, db));
+    CR_TRY(mat(q + "w_qkv", B.w_qkv, db, 3 * db, db));
+    CR_TRY(vec(q + "b_qkv", B.b_qkv, 3 * db));
+    CR_TRY(mat(q + "w_o", B.w_o, db, db, db));
+    CR_TRY(vec(q + "b_o", B.b_o, db));
+    CR_TRY(vec(q + "ln2_g", B.ln2_g, db));
+    CR_TRY(vec(q + "ln2_b", B.ln2_b, db));
+    CR_TRY(mat(q + "w_ff1", B.w_ff1, db, r * db, db));
+    CR_TRY(vec(q + "b_ff1", B.b_ff1, r * db));
+    CR_TRY(mat(q + "w_ff2", B.w_ff2, r * db, db, r * db));
+    CR_TRY(vec(q + "b_ff2", B.b_ff2, db));
+  }
+  CR_TRY(vec("ln_f_g", p.ln_f_g, db));
+  CR_TRY(vec("ln_f_b", p.ln_f_b, db));
+  CR_TRY(mat("w_out", p.w_out, db, D, db));
+  CR_TRY(vec("b_out", p.b_out, D));
+  CR_TRY(cr::convert_f32<float>(srcf("sigma_delta"), reinterpret_cast<float*>(out + p.sigma_delta),
+                                D, D, 1, 0, 0, s));
+  return CR_OK;
+}
+
+template <typename T>
+cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t n_chunks,
+                      const int32_t* req, int32_t n_req, const T* emb, const cr_dims* d,
+                      const char* prep, char* ws, int64_t N, int max_len, hipStream_t s) {
+  const Prepared P = prepared_layout(d, l);
+  const Workspace W = workspace_layout(d, l, N);
+  const int M = (int)N;
+  const int dc = d->d_c, db = d->d_b, E = d->d_model, r = d->ffn_mult, nh = d->n_heads;
+  const int dhd = db / nh;
+  const int S = 2 * l->n_layers * l->n_kv_heads, D = S * l->head_dim;
+  const int64_t ldst = W.ldst;
+  auto PT = [&](uint64_t o) { return reinterpret_cast<const T*>(prep + o); };
+  auto PF = [&](uint64_t o) { return reinterpret_cast<const float*>(prep + o); };
+  auto WT = [&](uint64_t o) { return reinterpret_cast<T*>(ws + o); };
+  int* lo = reinterpret_cast<int*>(ws + W.lo);
+  int* hi = reinterpret_cast<int*>(ws + W.hi);
+  int* pos = reinterpret_cast<int*>(ws + W.pos);
+  float2* rope = reinterpret_cast<float2*>(ws + W.rope);
+  T *U = WT(W.U), *st = WT(W.st), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q), *k = WT(W.k),
+    *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
+  const cr::KvStrides ks{l->stride_layer, l->stride_kv, l->stride_token, l->stride_head,
+                         l->n_kv_heads, l->head_dim};
+  const float eps = d->ln_eps;
+
+  CR_TRY(cr::chunk_schedule(off, n_chunks, req, n_req, lo, hi, pos, s));
+  CR_TRY(cr::rope_table(rope, max_len, dhd, (double)d->rope_theta, s));
+  // StaleEncoder: per-segment projections, compression, LN_enc -> s = st[:, :d_c]
+  CR_TRY(cr::compress_segments<T>(kv, ks, l->n_layers, PT(P.w_seg), PF(P.b_seg), U, P.kc_pad,
+                                  d->d_seg, M, s));
+  CR_TRY(cr::gemm_bias<T>(U, P.kc_pad, PT(P.w_cmp), P.kc_pad, M, dc, (int)P.kc_pad, st, ldst,
+                          PF(P.b_cmp), nullptr, 0, false, s));
+  CR_TRY(cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s));
+  // token projection -> st[:, d_c:], fusion -> h^0
+  CR_TRY(cr::gemm_bias<T>(emb, E, PT(P.w_tok), E, M, db, E, st + dc, ldst, PF(P.b_tok), nullptr,
+                          0, false, s));
+  CR_TRY(cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
+                          nullptr, 0, false, s));
+  for (int b = 0; b < d->n_blocks; ++b) {
+    const BlockP& B = P.blk[b];
+    CR_TRY(cr::gemm_bias<T>(st, ldst, PT(B.w_inj), dc, M, db, dc, h, db, PF(B.b_inj), h, db,
+                            false, s));
+    CR_TRY(cr::layernorm<T>(h, db, a, db, PF(B.ln1_g), PF(B.ln1_b), M, db, eps, s));
+    CR_TRY(cr::gemm_qkv<T>(a, db, PT(B.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(B.b_qkv),
+                           pos, rope, s));
+    CR_TRY(cr::attention<T>(q, k, vt, o, M, db, nh, dhd, W.n_pad, lo, hi, s));
+    CR_TRY(cr::gemm_bias<T>(o, db, PT(B.w_o), db, M, db, db, h, db, PF(B.b_o), h, db, false, s));
+    CR_TRY(cr::layernorm<T>(h, db, a, db, PF(B.ln2_g), PF(B.ln2_b), M, db, eps, s));
+    CR_TRY(cr::gemm_bias<T>(a, db, PT(B.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
+                            PF(B.b_ff1), nullptr, 0, true, s));
+    CR_TRY(cr::gemm_bias<T>(f, (int64_t)r * db, PT(B.w_ff2), (int64_t)r * db, M, db, r * db, h,
+                            db, PF(B.b_ff2), h, db, false, s));
+  }
+  CR_TRY(cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s));
+  CR_TRY(cr::gemm_expand<T>(a, db, PT(P.w_out), M, D, db, kv, ks, PF(P.b_out),
+                            PF(P.sigma_delta), s));
+  return CR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cr_version(void) { return CR_ABI_VERSION; }
+
+const char* cr_status_string(cr_status s) {
+  switch (s) {
+    case CR_OK: return "ok";
+    case CR_ERR_NULL: return "a required pointer is NULL";
+    case CR_ERR_DIMS: return "unsupported repairer or cache dimensions";
+    case CR_ERR_OFFSETS: return "malformed chunk_offsets or request_chunks";
+    case CR_ERR_LAYOUT: return "cache strides overlap, are misaligned or negative";
+    case CR_ERR_WORKSPACE: return "buffer too small or misaligned";
+    case CR_ERR_DTYPE: return "unknown storage dtype";
+    case CR_ERR_DEVICE: return "current device is not gfx950";
+    case CR_ERR_LAUNCH: return "kernel launch failed";
+    case CR_ERR_CAPACITY: return "descriptor table too small";
+    default: return "unknown status";
+  }
+}
+
+cr_status cr_weights_layout(const cr_dims* dims, const cr_kv_layout* layout,
+                            cr_tensor_desc* entries, int32_t max_entries, int32_t* n_entries,
+                            uint64_t* total_bytes) {
+  if (!dims || !layout || !n_entries || !total_bytes) return CR_ERR_NULL;
+  const cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  uint64_t total = 0;
+  const std::vector<Tensor> v = canonical(dims, layout, &total);
+  *n_entries = (int32_t)v.size();
+  *total_bytes = total;
+  if (!entries) return CR_OK;
+  if (max_entries < (int32_t)v.size()) return CR_ERR_CAPACITY;
+  for (size_t i = 0; i < v.size(); ++i) {
+    cr_tensor_desc& e = entries[i];
+    std::memset(&e, 0, sizeof(e));
+    std::strncpy(e.name, v[i].name.c_str(), CR_MAX_NAME - 1);
+    e.dtype = v[i].dtype;
+    e.ndim = (int32_t)v[i].shape.size();
+    for (int k = 0; k < e.ndim; ++k) e.shape[k] = v[i].shape[k];
+    e.offset_bytes = v[i].off;
+    e.nbytes = v[i].nbytes;
+  }
+  return CR_OK;
+}
+
+cr_status cr_prepared_bytes(const cr_dims* dims, const cr_kv_layout* layout, uint64_t* bytes) {
+  if (!dims || !layout || !bytes) return CR_ERR_NULL;
+  const cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  *bytes = prepared_layout(dims, layout).total;
+  return CR_OK;
+}
+
+cr_status cr_workspace_bytes(const cr_dims* dims, const cr_kv_layout* layout, int64_t n_tokens,
+                             uint64_t* bytes) {
+  if (!dims || !layout || !bytes) return CR_ERR_NULL;
+  const cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  if (n_tokens < 0 || n_tokens >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  *bytes = workspace_layout(dims, layout, n_tokens).total;
+  return CR_OK;
+}
+
+cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layout, int64_t n_tokens,
+                            const char* name, uint64_t* offset_bytes, int64_t* row_stride) {
+  if (!dims || !layout || !name || !offset_bytes || !row_stride) return CR_ERR_NULL;
+  const cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  const Workspace w = workspace_layout(dims, layout, n_tokens);
+  if (!std::strcmp(name, "s")) { *offset_bytes = w.st; *row_stride = w.ldst; }
+  else if (!std::strcmp(name, "h")) { *offset_bytes = w.h; *row_stride = dims->d_b; }
+  else if (!std::strcmp(name, "lnf")) { *offset_bytes = w.a; *row_stride = dims->d_b; }
+  else return CR_ERR_DIMS;
+  return CR_OK;
+}
+
+cr_status cr_prepare_weights(const cr_dims* dims, const cr_kv_layout* layout, const void* blob,
+                             uint64_t blob_bytes, void* prepared, uint64_t prepared_bytes,
+                             void* stream) {
+  if (!dims || !layout || !blob || !prepared) return CR_ERR_NULL;
+  cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  uint64_t need = 0;
+  canonical(dims, layout, &need);
+  if (blob_bytes < need || !aligned(blob, ALIGN)) return CR_ERR_WORKSPACE;
+  if (prepared_bytes < prepared_layout(dims, layout).total || !aligned(prepared, ALIGN))
+    return CR_ERR_WORKSPACE;
+  st = check_device();
+  if (st != CR_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (layout->dtype == CR_DTYPE_BF16)
+    return prepare_impl<bf16>(dims, layout, static_cast<const char*>(blob),
+                              static_cast<char*>(prepared), s);
+  return prepare_impl<float>(dims, layout, static_cast<const char*>(blob),
+                             static_cast<char*>(prepared), s);
+}
+
+cr_status cr_chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
+                            const int32_t* request_chunks, int32_t n_requests, int32_t* rows,
+                            void* stream) {
+  if (!rows) return CR_ERR_NULL;
+  cr_status st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
+  if (st != CR_OK) return st;
+  const int64_t N = chunk_offsets[n_chunks];
+  if (N == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (cr::chunk_schedule(chunk_offsets, n_chunks, request_chunks, n_requests, rows, rows + N,
+                         rows + 2 * N, s) != hipSuccess)
+    return CR_ERR_LAUNCH;
+  return CR_OK;
+}
+
+cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                    int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                    const void* token_embeds, const cr_dims* dims, const void* prepared,
+                    uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
+                    void* stream) {
+  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace) return CR_ERR_NULL;
+  cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
+  if (st != CR_OK) return st;
+  const int64_t N = chunk_offsets[n_chunks];
+  if (N >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  st = check_layout(layout, N);
+  if (st != CR_OK) return st;
+  if (!aligned(kv, 16) || !aligned(token_embeds, 16)) return CR_ERR_LAYOUT;
+  if (prepared_bytes < prepared_layout(dims, layout).total || !aligned(prepared, ALIGN))
+    return CR_ERR_WORKSPACE;
+  if (workspace_bytes < workspace_layout(dims, layout, N).total || !aligned(workspace, ALIGN))
+    return CR_ERR_WORKSPACE;
+  if (N == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  int max_len = 0;
+  if (request_chunks) {
+    for (int r = 0; r < n_requests; ++r)
+      max_len = std::max(max_len, chunk_offsets[request_chunks[r + 1]] -
+                                      chunk_offsets[request_chunks[r]]);
+  } else {
+    max_len = (int)N;
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (layout->dtype == CR_DTYPE_BF16)
+    return repair_impl<bf16>(static_cast<bf16*>(kv), layout, chunk_offsets, n_chunks,
+                             request_chunks, n_requests, static_cast<const bf16*>(token_embeds),
+                             dims, static_cast<const char*>(prepared),
+                             static_cast<char*>(workspace), N, max_len, s);
+  return repair_impl<float>(static_cast<float*>(kv), layout, chunk_offsets, n_chunks,
+                            request_chunks, n_requests, static_cast<const float*>(token_embeds),
+                            dims, static_cast<const char*>(prepared),
+                            static_cast<char*>(workspace), N, max_len, s);
+}
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// Host-side launchers of the CacheRepair kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace cr {
+
+// Cache layout as seen by the kernels (elements).
+struct KvStrides {
+  int64_t layer, kv, token, head;
+  int n_kv_heads, head_dim;
+};
+
+// ---- GEMM: C[M][N] = A[M][K] * B[N][K]^T, fp32 accumulation, K % 64 == 0.
+// Bias / GELU / residual epilogue: out = act(acc + bias) (+ resid).
+template <typename T>
+hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
+                     T* out, int64_t ldo, const float* bias, const T* resid, int64_t ldr,
+                     bool gelu, hipStream_t s);
+
+// QKV projection with the repair backbone's RoPE on Q and K (rotate-half
+// pairs, table rope[pos][d_head/2] of (cos, sin)); V is written transposed,
+// vt[head][d][n_pad].
+template <typename T>
+hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
+                    T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
+                    const float2* rope, hipStream_t s);
+
+// KV residual head fused with the in-place add into the strided cache:
+// kv[t, j] += sigma[j] * (acc[t, j] + bias[j]) for j in [0, D_KV).
+template <typename T>
+hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K, T* kv,
+                       KvStrides ks, const float* bias, const float* sigma, hipStream_t s);
+
+// ---- block-causal flash attention (per-row key interval [lo, hi)).
+template <typename T>
+hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, int n_heads,
+                     int d_head, int64_t n_pad, const int* lo, const int* hi, hipStream_t s);
+
+// ---- row LayerNorm, C % 8 == 0, C <= 2048.
+template <typename T>
+hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g, const float* b,
+                     int M, int C, float eps, hipStream_t s);
+
+// ---- StaleEncoder stage 1: per-segment projections of the scaled cache into
+// U[N][ldu] (segment-major columns g*d_seg + j; columns [S*d_seg, ldu) zeroed).
+template <typename T>
+hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* wseg,
+                             const float* bseg, T* U, int64_t ldu, int d_seg, int N,
+                             hipStream_t s);
+
+// ---- chunk schedule: lo/hi/pos per token from host chunk structure.
+hipError_t chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
+                          const int32_t* request_chunks, int32_t n_requests, int* lo, int* hi,
+                          int* pos, hipStream_t s);
+
+// ---- RoPE (cos, sin) table for positions [0, max_pos), computed in fp64.
+hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStream_t s);
+
+// ---- weight preparation
+// dst[b][c][r] = src[b][r][c] / div[b][r] for r < R, c < C; zero for
+// r in [R, ld_dst) and c in [C, Cp).
+template <typename Tin, typename Tout>
+hipError_t transpose_convert(const Tin* src, Tout* dst, int batch, int R, int C, int Cp,
+                             int64_t ld_dst, const float* div, hipStream_t s);
+template <typename Tin>
+hipError_t convert_f32(const Tin* src, float* dst, int64_t n, int64_t n_pad, int batch,
+                       int64_t src_bstride, int64_t dst_bstride, hipStream_t s);
+
+}  // namespace cr

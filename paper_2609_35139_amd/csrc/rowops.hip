@@ -1,0 +1,264 @@
+// Row-wise and setup kernels of the repair forward pass (gfx950):
+//  - LayerNorm with wavefront reductions (one wave per row),
+//  - StaleEncoder stage 1 (per-segment projections streaming the cache),
+//  - the chunk schedule of the block-causal mask,
+//  - the RoPE (cos, sin) table,
+//  - one-time weight preparation (transpose / widen).
+#include <algorithm>
+#include <vector>
+
+#include "launch.h"
+
+namespace cr {
+
+// ------------------------------------------------------------- LayerNorm
+// y = (x - mean) / sqrt(var + eps) * g + b over rows of C elements, biased
+// variance, statistics in fp32 from values held in registers (two passes).
+template <typename T>
+__global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x, int64_t ldx,
+                                                        T* __restrict__ y, int64_t ldy,
+                                                        const float* __restrict__ g,
+                                                        const float* __restrict__ b, int M,
+                                                        int C, float eps) {
+  constexpr int MAXV = 4;  // 4 x 8 values per lane: C <= 2048
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const T* xr = x + (int64_t)row * ldx;
+  float v[MAXV][8];
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < C) {
+      Vec8<T> t; t.load(xr + c); t.to_float(v[k]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += v[k][e];
+    }
+  }
+  const float mean = wave_sum(sum) / (float)C;
+  float sq = 0.f;
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < C) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { const float d = v[k][e] - mean; sq += d * d; }
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)C + eps);
+  T* yr = y + (int64_t)row * ldy;
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < C) {
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (v[k][e] - mean) * rstd * g[c + e] + b[c + e];
+      Vec8<T> t; t.from_float(o); t.store(yr + c);
+    }
+  }
+}
+
+template <typename T>
+hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g, const float* b,
+                     int M, int C, float eps, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL((layernorm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
+                     g, b, M, C, eps);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- StaleEncoder stage 1
+// u_g = (x_g / sigma_g) W1_g + b1_g for every segment g = (l, kv, h), with
+// 1/sigma folded into the prepared weights wseg[g][32][d_h] (rows >= d_seg
+// are zero).  One workgroup = 64 tokens of one segment, 16 tokens per wave,
+// 16x16 MFMA atoms fed straight from the cache rows (each lane reads one
+// 16-byte run of a token's head vector).
+template <typename T>
+__global__ __launch_bounds__(256) void compress_segments_kernel(
+    const T* __restrict__ kv, KvStrides ks, const T* __restrict__ wseg,
+    const float* __restrict__ bseg, T* __restrict__ U, int64_t ldu, int d_seg, int N, int Kc) {
+  using MM = Mma16<T>;
+  using frag = typename MM::frag;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = blockIdx.y;
+  const int dh = ks.head_dim;
+  const int h = g % ks.n_kv_heads, lk = g / ks.n_kv_heads;
+  const T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
+                  (int64_t)h * ks.head;
+  const int t0 = blockIdx.x * 64 + wave * 16;
+  const int tr = t0 + (lane & 15);
+  const int fk = (lane >> 4) * MM::KPL;
+  const T* wg = wseg + (int64_t)g * 32 * dh;
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  for (int k0 = 0; k0 < dh; k0 += MM::KSTEP) {
+    const frag a = tr < N ? load_frag<T, frag>(base + (int64_t)tr * ks.token + k0 + fk) : frag{};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const frag bw = load_frag<T, frag>(wg + (j * 16 + (lane & 15)) * dh + k0 + fk);
+      acc[j] = MM::mma(a, bw, acc[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int col = j * 16 + (lane & 15);
+    if (col < d_seg) {
+      const float bb = bseg[g * 32 + col];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int t = t0 + (lane >> 4) * 4 + e;
+        if (t < N) U[(int64_t)t * ldu + g * d_seg + col] = from_f32<T>(acc[j][e] + bb);
+      }
+    }
+  }
+  if (g == 0) {  // zero the K padding of U for this wave's tokens
+    for (int idx = lane; idx < 16 * (ldu - Kc); idx += 64) {
+      const int t = t0 + idx / (int)(ldu - Kc);
+      const int c = Kc + idx % (int)(ldu - Kc);
+      if (t < N) U[(int64_t)t * ldu + c] = from_f32<T>(0.f);
+    }
+  }
+}
+
+template <typename T>
+hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* wseg,
+                             const float* bseg, T* U, int64_t ldu, int d_seg, int N,
+                             hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  const int S = 2 * n_layers * ks.n_kv_heads;
+  dim3 grid((N + 63) / 64, S);
+  hipLaunchKernelGGL((compress_segments_kernel<T>), grid, dim3(256), 0, s, kv, ks, wseg, bseg, U,
+                     ldu, d_seg, N, S * d_seg);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------- chunk schedule
+constexpr int SCHED_CHUNKS = 256;
+struct SchedBatch {
+  int count;                      // chunks in this batch
+  int offs[SCHED_CHUNKS + 1];     // token offsets of the batch's chunks
+  int req_start[SCHED_CHUNKS];    // first token of each chunk's request
+};
+
+__global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __restrict__ lo,
+                                                       int* __restrict__ hi,
+                                                       int* __restrict__ pos) {
+  const int t = sb.offs[0] + blockIdx.x * 256 + threadIdx.x;
+  if (t >= sb.offs[sb.count]) return;
+  // largest c with offs[c] <= t (skips empty chunks)
+  int a = 0, b = sb.count;
+  while (b - a > 1) {
+    const int mid = (a + b) >> 1;
+    if (sb.offs[mid] <= t) a = mid; else b = mid;
+  }
+  lo[t] = sb.req_start[a];
+  hi[t] = sb.offs[a + 1];
+  pos[t] = t - sb.req_start[a];
+}
+
+hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* req,
+                          int32_t n_req, int* lo, int* hi, int* pos, hipStream_t s) {
+  std::vector<int> rs(n_chunks);
+  if (req == nullptr) {
+    std::fill(rs.begin(), rs.end(), off[0]);
+  } else {
+    for (int r = 0; r < n_req; ++r)
+      for (int c = req[r]; c < req[r + 1]; ++c) rs[c] = off[req[r]];
+  }
+  for (int c0 = 0; c0 < n_chunks; c0 += SCHED_CHUNKS) {
+    SchedBatch sb;
+    sb.count = std::min(SCHED_CHUNKS, n_chunks - c0);
+    for (int i = 0; i <= sb.count; ++i) sb.offs[i] = off[c0 + i];
+    for (int i = 0; i < sb.count; ++i) sb.req_start[i] = rs[c0 + i];
+    const int ntok = sb.offs[sb.count] - sb.offs[0];
+    if (ntok == 0) continue;
+    hipLaunchKernelGGL(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// ------------------------------------------------------------ RoPE table
+__global__ __launch_bounds__(256) void rope_table_kernel(float2* tab, int max_pos, int half,
+                                                         int d_head, double theta) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= max_pos * half) return;
+  const int p = idx / half, i = idx % half;
+  const double ang = (double)p * pow(theta, -2.0 * (double)i / (double)d_head);
+  tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStream_t s) {
+  const int half = d_head / 2;
+  const int n = max_pos * half;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos,
+                     half, d_head, theta);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- weight preparation
+template <typename Tin, typename Tout>
+__global__ __launch_bounds__(256) void transpose_convert_kernel(const Tin* __restrict__ src,
+                                                                Tout* __restrict__ dst, int R,
+                                                                int C, int Cp, int64_t ld_dst,
+                                                                const float* __restrict__ div) {
+  const int b = blockIdx.z;
+  const int64_t n = (int64_t)Cp * ld_dst;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= n) return;
+  const int c = (int)(idx / ld_dst), r = (int)(idx % ld_dst);
+  float v = 0.f;
+  if (c < C && r < R) {
+    v = to_f32(src[(int64_t)b * R * C + (int64_t)r * C + c]);
+    if (div) v = v / div[(int64_t)b * R + r];
+  }
+  dst[(int64_t)b * n + idx] = from_f32<Tout>(v);
+}
+
+template <typename Tin, typename Tout>
+hipError_t transpose_convert(const Tin* src, Tout* dst, int batch, int R, int C, int Cp,
+                             int64_t ld_dst, const float* div, hipStream_t s) {
+  const int64_t n = (int64_t)Cp * ld_dst;
+  if (n <= 0 || batch <= 0) return hipSuccess;
+  dim3 grid((unsigned)((n + 255) / 256), 1, batch);
+  hipLaunchKernelGGL((transpose_convert_kernel<Tin, Tout>), grid, dim3(256), 0, s, src, dst, R, C,
+                     Cp, ld_dst, div);
+  return hipGetLastError();
+}
+
+template <typename Tin>
+__global__ __launch_bounds__(256) void convert_f32_kernel(const Tin* __restrict__ src,
+                                                          float* __restrict__ dst, int64_t n,
+                                                          int64_t n_pad, int64_t sb, int64_t db) {
+  const int b = blockIdx.z;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pad) return;
+  dst[b * db + i] = i < n ? to_f32(src[b * sb + i]) : 0.f;
+}
+
+template <typename Tin>
+hipError_t convert_f32(const Tin* src, float* dst, int64_t n, int64_t n_pad, int batch,
+                       int64_t sb, int64_t db, hipStream_t s) {
+  if (n_pad <= 0 || batch <= 0) return hipSuccess;
+  dim3 grid((unsigned)((n_pad + 255) / 256), 1, batch);
+  hipLaunchKernelGGL((convert_f32_kernel<Tin>), grid, dim3(256), 0, s, src, dst, n, n_pad, sb, db);
+  return hipGetLastError();
+}
+
+#define CR_INST(T)                                                                               \
+  template hipError_t layernorm<T>(const T*, int64_t, T*, int64_t, const float*, const float*,  \
+                                   int, int, float, hipStream_t);                               \
+  template hipError_t compress_segments<T>(const T*, KvStrides, int, const T*, const float*, T*, \
+                                           int64_t, int, int, hipStream_t);                     \
+  template hipError_t transpose_convert<T, T>(const T*, T*, int, int, int, int, int64_t,        \
+                                              const float*, hipStream_t);                       \
+  template hipError_t convert_f32<T>(const T*, float*, int64_t, int64_t, int, int64_t, int64_t, \
+                                     hipStream_t);
+CR_INST(bf16)
+CR_INST(float)
+#undef CR_INST
+
+}  // namespace cr

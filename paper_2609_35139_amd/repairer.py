@@ -1,0 +1,83 @@
+"""Torch-side marshalling around the C ABI: device buffers and streams only.
+
+:class:`Repairer` packs a repairer's named weights into the canonical blob
+described by ``cr_weights_layout``, runs the one-time ``cr_prepare_weights``
+and then calls ``cr_repair`` on caller-owned caches.  Every arithmetic step
+of the repair runs in the HIP library; this module only allocates device
+memory, copies host arrays in and passes pointers.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+TORCH_DTYPE = {B.CR_DTYPE_BF16: torch.bfloat16, B.CR_DTYPE_F32: torch.float32}
+
+
+def storage_dtype(name: str) -> int:
+    return {"bf16": B.CR_DTYPE_BF16, "f32": B.CR_DTYPE_F32}[name]
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Repairer:
+    """Prepared repairer weights on one device."""
+
+    def __init__(self, dims: B.cr_dims, n_layers: int, n_kv_heads: int, head_dim: int,
+                 dtype: int, weights: Dict[str, np.ndarray], device="cuda",
+                 stream: Optional[torch.cuda.Stream] = None):
+        B.load()
+        self.dims = dims
+        self.dtype = dtype
+        self.shape = (n_layers, n_kv_heads, head_dim)
+        self.device = torch.device(device)
+        # layout strides do not change buffer sizes; a 1-token layout describes them
+        lay = B.layer_major_layout(n_layers, n_kv_heads, head_dim, 1, dtype)
+        descs, total = B.cr_weights_layout(dims, lay)
+        blob = np.zeros(total, np.uint8)
+        for d in descs:
+            arr = np.asarray(weights[d["name"]], np.float32)
+            if arr.shape != tuple(d["shape"]):
+                raise ValueError(f"{d['name']}: shape {arr.shape} != {d['shape']}")
+            t = torch.from_numpy(np.ascontiguousarray(arr)).to(TORCH_DTYPE[d["dtype"]])
+            raw = t.view(torch.uint8).numpy() if d["dtype"] == B.CR_DTYPE_F32 else \
+                t.view(torch.int16).numpy().view(np.uint8)
+            blob[d["offset_bytes"]:d["offset_bytes"] + d["nbytes"]] = raw.reshape(-1)
+        self.blob = torch.from_numpy(blob).to(self.device)
+        self.prepared_bytes = B.cr_prepared_bytes(dims, lay)
+        self.prepared = torch.empty(self.prepared_bytes, dtype=torch.uint8, device=self.device)
+        B.cr_prepare_weights(dims, lay, self.blob.data_ptr(), total, self.prepared.data_ptr(),
+                             self.prepared_bytes, _stream_handle(stream))
+
+    def layout(self, n_tokens: int) -> B.cr_kv_layout:
+        L, H, dh = self.shape
+        return B.layer_major_layout(L, H, dh, n_tokens, self.dtype)
+
+    def workspace(self, n_tokens: int) -> torch.Tensor:
+        n = B.cr_workspace_bytes(self.dims, self.layout(n_tokens), n_tokens)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=self.device)
+
+    def repair(self, kv: torch.Tensor, chunk_offsets: Sequence[int],
+               request_chunks: Optional[Sequence[int]], token_embeds: torch.Tensor,
+               workspace: Optional[torch.Tensor] = None,
+               layout: Optional[B.cr_kv_layout] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """Repair ``kv`` in place (layer-major [L][2][N][H][d_h] unless a layout is given)."""
+        n = int(chunk_offsets[-1])
+        lay = layout if layout is not None else self.layout(n)
+        ws = workspace if workspace is not None else self.workspace(n)
+        if kv.dtype != TORCH_DTYPE[self.dtype] or token_embeds.dtype != TORCH_DTYPE[self.dtype]:
+            raise TypeError("kv and token_embeds must use the repairer's storage dtype")
+        if not token_embeds.is_contiguous() or token_embeds.shape != (n, self.dims.d_model):
+            raise ValueError("token_embeds must be a contiguous [N, d_model] tensor")
+        B.cr_repair(kv.data_ptr(), lay, chunk_offsets, request_chunks, token_embeds.data_ptr(),
+                    self.dims, self.prepared.data_ptr(), self.prepared_bytes, ws.data_ptr(),
+                    ws.numel(), _stream_handle(stream))
+        return kv

@@ -1,0 +1,177 @@
+"""CPU tests of the C ABI: exported symbols, layouts and host-side validation.
+
+Every call here returns before anything is enqueued, so no GPU is needed.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+from paper_2609_35139_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cacherepair.h")
+
+
+def _dims(w):
+    t, r = w.target, w.rep
+    return B.make_dims(t.d_model, r.d_seg, r.d_c, r.d_b, r.n_blocks, r.n_heads, r.ffn_mult,
+                       r.rope_theta, r.ln_eps)
+
+
+def _layout(w, n=None, dtype=None):
+    t = w.target
+    dt = dtype if dtype is not None else (B.CR_DTYPE_BF16 if w.dtype == "bf16" else B.CR_DTYPE_F32)
+    return B.layer_major_layout(t.n_layers, t.n_kv_heads, t.head_dim,
+                                w.n_tokens if n is None else n, dt)
+
+
+def test_library_exports_every_declared_symbol():
+    decl = re.findall(r"CR_API\s+[\w\s\*]+?\b(cr_\w+)\s*\(", open(HEADER).read())
+    assert sorted(decl) == sorted(B.EXPORTS)
+    lib = B.load()
+    for name in decl:
+        assert hasattr(lib, name), name
+    assert B.cr_version() == 1
+    assert B.cr_status_string(0) == "ok"
+    assert "offsets" in B.cr_status_string(-3)
+
+
+def test_struct_sizes_match_c():
+    assert ctypes.sizeof(B.cr_kv_layout) == 48
+    assert ctypes.sizeof(B.cr_dims) == 36
+    assert ctypes.sizeof(B.cr_tensor_desc) == 48 + 8 + 32 + 16
+
+
+@pytest.mark.parametrize("i", range(5))
+def test_weights_layout_matches_inventory(i):
+    w = W.WORKLOADS[i]
+    descs, total = B.cr_weights_layout(_dims(w), _layout(w))
+    inv = W.param_inventory(w.target, w.rep)
+    assert [d["name"] for d in descs] == [n for n, _, _ in inv]
+    assert [tuple(d["shape"]) for d in descs] == [s for _, s, _ in inv]
+    esz = 2 if w.dtype == "bf16" else 4
+    prev_end = 0
+    for d, (_, shape, kind) in zip(descs, inv):
+        assert d["offset_bytes"] % 256 == 0 and d["offset_bytes"] >= prev_end
+        sz = 4 if kind == "sigma" else esz
+        assert d["nbytes"] == int(np.prod(shape)) * sz
+        prev_end = d["offset_bytes"] + d["nbytes"]
+    assert total >= prev_end
+    assert B.cr_prepared_bytes(_dims(w), _layout(w)) > 0
+    assert B.cr_workspace_bytes(_dims(w), _layout(w), w.n_tokens) > 0
+
+
+def _call_repair(w, kv=0x10000, emb=0x20000, prep=0x30000, ws=0x40000, offsets=None,
+                 req="default", dims=None, layout=None, ws_bytes=None, prep_bytes=None):
+    dims = dims or _dims(w)
+    layout = layout or _layout(w)
+    offsets = w.chunk_offsets if offsets is None else offsets
+    req = w.request_chunks if isinstance(req, str) else req
+    n = int(offsets[-1]) if len(offsets) else 0
+    if ws_bytes is None:
+        ws_bytes = B.cr_workspace_bytes(_dims(w), _layout(w), max(n, 0))
+    if prep_bytes is None:
+        prep_bytes = B.cr_prepared_bytes(_dims(w), _layout(w))
+    with pytest.raises(B.CrError) as e:
+        B.cr_repair(kv, layout, offsets, req, emb, dims, prep, prep_bytes, ws, ws_bytes, None)
+    return e.value.name
+
+
+W0 = W.WORKLOADS[0]
+
+
+def test_null_pointers():
+    assert _call_repair(W0, kv=0) == "CR_ERR_NULL"
+    assert _call_repair(W0, emb=0) == "CR_ERR_NULL"
+    assert _call_repair(W0, prep=0) == "CR_ERR_NULL"
+    assert _call_repair(W0, ws=0) == "CR_ERR_NULL"
+
+
+@pytest.mark.parametrize("offsets,req", [
+    ([1, 32, 64], [0, 2]),          # does not start at 0
+    ([0, 40, 32], [0, 2]),          # decreasing
+    ([0, 32, 64], [0, 1]),          # requests do not cover every chunk
+    ([0, 32, 64], [1, 2]),          # requests do not start at chunk 0
+    ([0, 32, 64], [0, 2, 1]),       # decreasing request offsets
+    ([0], [0, 0]),                  # no chunks
+])
+def test_bad_offsets(offsets, req):
+    assert _call_repair(W0, offsets=np.array(offsets), req=np.array(req)) == "CR_ERR_OFFSETS"
+
+
+def test_bad_dims():
+    t = W0.target
+    base = dict(d_model=t.d_model, d_seg=8, d_c=64, d_b=128, n_blocks=2, n_heads=4, ffn_mult=4)
+    for change in [dict(n_heads=3), dict(n_heads=1), dict(d_seg=33), dict(d_seg=0),
+                   dict(d_c=96), dict(d_b=192), dict(d_model=100), dict(ffn_mult=0),
+                   dict(n_blocks=-1)]:
+        kw = dict(base, **change)
+        d = B.make_dims(**kw)
+        assert _call_repair(W0, dims=d) == "CR_ERR_DIMS", change
+
+
+def test_bad_dtype():
+    lay = _layout(W0)
+    lay.dtype = 7
+    assert _call_repair(W0, layout=lay) == "CR_ERR_DTYPE"
+
+
+def test_bad_layouts():
+    t = W0.target
+    good = _layout(W0)
+    overlap = _layout(W0)
+    overlap.stride_token = 8          # tokens overlap a head vector
+    assert _call_repair(W0, layout=overlap) == "CR_ERR_LAYOUT"
+    odd = _layout(W0)
+    odd.stride_head = 68              # not a multiple of 8 elements
+    odd.stride_token = 2 * 68
+    assert _call_repair(W0, layout=odd) == "CR_ERR_LAYOUT"
+    neg = _layout(W0)
+    neg.stride_layer = -good.stride_layer
+    assert _call_repair(W0, layout=neg) == "CR_ERR_LAYOUT"
+    assert _call_repair(W0, kv=0x10002) == "CR_ERR_LAYOUT"   # misaligned cache pointer
+    small_head = _layout(W0)
+    small_head.head_dim = 48
+    assert _call_repair(W0, layout=small_head) == "CR_ERR_DIMS"
+
+
+def test_workspace_and_prepared_checks():
+    need = B.cr_workspace_bytes(_dims(W0), _layout(W0), W0.n_tokens)
+    assert _call_repair(W0, ws_bytes=need - 1) == "CR_ERR_WORKSPACE"
+    assert _call_repair(W0, ws=0x40080) == "CR_ERR_WORKSPACE"     # not 256-byte aligned
+    pb = B.cr_prepared_bytes(_dims(W0), _layout(W0))
+    assert _call_repair(W0, prep_bytes=pb - 1) == "CR_ERR_WORKSPACE"
+
+
+def test_empty_batch_is_a_no_op():
+    # all chunks empty: N == 0 returns OK before touching any device state
+    B.cr_repair(0x10000, _layout(W0, n=0), np.array([0, 0, 0]), np.array([0, 2]), 0x20000,
+                _dims(W0), 0x30000, B.cr_prepared_bytes(_dims(W0), _layout(W0)), 0x40000,
+                B.cr_workspace_bytes(_dims(W0), _layout(W0), 0), None)
+
+
+def test_schedule_and_prepare_validation():
+    with pytest.raises(B.CrError) as e:
+        B.cr_chunk_schedule([0, 5, 3], None, 0x1000)
+    assert e.value.name == "CR_ERR_OFFSETS"
+    with pytest.raises(B.CrError) as e:
+        B.cr_chunk_schedule([0, 5], None, 0)
+    assert e.value.name == "CR_ERR_NULL"
+    _, total = B.cr_weights_layout(_dims(W0), _layout(W0))
+    pb = B.cr_prepared_bytes(_dims(W0), _layout(W0))
+    with pytest.raises(B.CrError) as e:
+        B.cr_prepare_weights(_dims(W0), _layout(W0), 0x1000, total - 1, 0x100000, pb)
+    assert e.value.name == "CR_ERR_WORKSPACE"
+
+
+def test_workspace_views():
+    off_s, ld_s = B.cr_workspace_view(_dims(W0), _layout(W0), 64, "s")
+    off_h, ld_h = B.cr_workspace_view(_dims(W0), _layout(W0), 64, "h")
+    assert ld_s == W0.rep.d_c + W0.rep.d_b and ld_h == W0.rep.d_b
+    assert off_s % 256 == 0 and off_h % 256 == 0 and off_s != off_h
+    with pytest.raises(B.CrError):
+        B.cr_workspace_view(_dims(W0), _layout(W0), 64, "nope")

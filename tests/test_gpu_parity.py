@@ -1,0 +1,170 @@
+"""GPU parity of the HIP repair path against the fp64 oracle (through the C ABI)."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from helpers import (assert_parity, gpu_repair, oracle_repair, repairer_for, small_workload,
+                     to_device, truncate_requests)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35139_amd import binding
+    binding.load()
+
+
+# ------------------------------------------------------------- schedule
+@pytest.mark.parametrize("lengths", [
+    ((32, 32),),
+    ((70, 0, 133), (5, 61)),
+    ((1,) * 300,),                                  # more chunks than one launch batch
+    tuple(tuple(int(x) for x in r) for r in np.random.default_rng(3).integers(0, 40, (5, 70))),
+])
+def test_chunk_schedule_is_exact(lengths):
+    import torch
+    from paper_2609_35139_amd import binding as B
+    w = small_workload(lengths)
+    off, rc = w.chunk_offsets, w.request_chunks
+    n = int(off[-1])
+    rows = torch.full((3 * n,), -7, dtype=torch.int32, device="cuda")
+    B.cr_chunk_schedule(off, rc, rows.data_ptr())
+    torch.cuda.synchronize()
+    got = rows.cpu().numpy().reshape(3, n)
+    c = O.token_chunk_ids(off)
+    r = O.token_request_ids(off, rc)
+    lo = np.array([off[rc[r[t]]] for t in range(n)])
+    hi = np.array([off[c[t] + 1] for t in range(n)])
+    assert np.array_equal(got[0], lo)
+    assert np.array_equal(got[1], hi)
+    assert np.array_equal(got[2], O.positions(off, rc))
+    # the interval [lo, hi) is exactly row t of the mask A_ij
+    if n <= 400:
+        allowed = O.block_causal_allowed(c, r)
+        j = np.arange(n)
+        iv = (j[None, :] >= got[0][:, None]) & (j[None, :] < got[1][:, None])
+        assert np.array_equal(iv, allowed)
+
+
+# ------------------------------------------------------------ small parity
+SMALL = [
+    dict(lengths=((70, 0, 133), (5, 61)), dtype="f32", L=2, H=2, dh=64, E=128, d_c=64, d_b=128,
+         n_heads=4, d_seg=8),
+    dict(lengths=((70, 0, 133), (5, 61)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64, d_b=128,
+         n_heads=2, d_seg=8),
+    dict(lengths=((129, 1, 200),), dtype="bf16", L=3, H=1, dh=128, E=192, d_c=128, d_b=256,
+         n_heads=4, d_seg=24, n_blocks=3),
+    dict(lengths=((1,), (2, 3), (64,)), dtype="f32", L=1, H=1, dh=32, E=64, d_c=64, d_b=128,
+         n_heads=2, d_seg=32),
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=[f"small{i}" for i in range(len(SMALL))])
+def test_parity_small(cfg):
+    cfg = dict(cfg)
+    w = small_workload(cfg.pop("lengths"), seed=5, ffn_mult=4, n_blocks=cfg.pop("n_blocks", 2),
+                       **cfg)
+    inp = W.make_inputs(w)
+    Y = gpu_repair(inp)
+    assert_parity(Y, oracle_repair(inp), W.kv_layer_major_to_canonical(inp.kv), w)
+
+
+@pytest.mark.parametrize("i", [0, 1])
+def test_parity_workload_full(i):
+    w = W.WORKLOADS[i]
+    inp = W.make_inputs(w)
+    Y = gpu_repair(inp)
+    assert_parity(Y, oracle_repair(inp), W.kv_layer_major_to_canonical(inp.kv), w)
+
+
+# ------------------------------------------------------------ invariants
+def test_zero_head_is_bit_exact():
+    w = W.WORKLOADS[1]
+    inp = W.make_inputs(w)
+    wz = dict(inp.weights)
+    wz["w_out"] = np.zeros_like(wz["w_out"])
+    wz["b_out"] = np.zeros_like(wz["b_out"])
+    Y = gpu_repair(inp, weights=wz)
+    assert np.array_equal(Y, W.kv_layer_major_to_canonical(inp.kv))
+
+
+def test_prefix_independence_is_bit_exact():
+    w = small_workload(((100, 60, 90, 40),), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
+                       d_b=128, n_heads=2, d_seg=8, ffn_mult=4)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    Y0 = gpu_repair(inp, rep=rep)
+    off = w.chunk_offsets
+    for k in (1, 2, 3):
+        kv = inp.kv.copy()
+        kv[:, :, off[k]:] = W.round_to_storage(kv[:, :, off[k]:] * -1.5 + 0.25, "bf16")
+        emb = inp.token_embeds.copy()
+        emb[off[k]:] = 0.5
+        Y1 = gpu_repair(inp, kv=kv, embeds=emb, rep=rep)
+        assert np.array_equal(Y0[:off[k]], Y1[:off[k]]), k
+        assert not np.array_equal(Y0[off[k]:], Y1[off[k]:])
+
+
+def test_request_independence():
+    lengths = ((100, 60), (90, 40, 33))
+    w = small_workload(lengths, dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64, d_b=128,
+                       n_heads=2, d_seg=8, ffn_mult=4)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    Yp = gpu_repair(inp, rep=rep)
+    n0 = sum(lengths[0])
+    for rows, lens in ((slice(0, n0), lengths[0]), (slice(n0, None), lengths[1])):
+        off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        Ys = gpu_repair(inp, kv=inp.kv[:, :, rows], embeds=inp.token_embeds[rows], offsets=off,
+                        requests=None, rep=rep)
+        X = W.kv_layer_major_to_canonical(inp.kv[:, :, rows])
+        # tile boundaries shift with the request offset, so bf16 rounding
+        # differs; both must agree to the parity bound on the residual
+        d = np.abs(Ys - Yp[rows]).max()
+        assert d <= 5e-2 * np.abs(Ys - X).max(), d
+        ref = O.repair(W.kv_layer_major_to_canonical(inp.kv[:, :, rows]),
+                       inp.token_embeds[rows], off, None, inp.weights, w.target.head_dim,
+                       w.rep.n_heads)
+        assert np.abs(Ys - ref).max() <= 5e-2 * np.abs(ref - X).max()
+
+
+def test_run_to_run_determinism():
+    w = W.WORKLOADS[1]
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    assert np.array_equal(gpu_repair(inp, rep=rep), gpu_repair(inp, rep=rep))
+
+
+def test_layouts_give_identical_results():
+    """Layer-major, token-major and padded strides repair identically."""
+    import torch
+    from paper_2609_35139_amd import binding as B
+    from helpers import dims_of
+    w = small_workload(((70, 133),), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64, d_b=128,
+                       n_heads=2, d_seg=8, ffn_mult=4)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    ref = gpu_repair(inp, rep=rep)
+    L, H, dh, N = 2, 2, 64, w.n_tokens
+    emb = to_device(w, inp.token_embeds)
+    # token-major [N][L][2][H][dh]
+    tm = to_device(w, np.ascontiguousarray(inp.kv.transpose(2, 0, 1, 3, 4)))
+    lay = B.cr_kv_layout(L, H, dh, B.CR_DTYPE_BF16, 2 * H * dh, H * dh, L * 2 * H * dh, dh)
+    rep.repair(tm, w.chunk_offsets, w.request_chunks, emb, layout=lay)
+    # padded: [L][2][N][H][dh + 16] inside a larger buffer
+    pad = torch.zeros((L, 2, N, H, dh + 16), dtype=torch.bfloat16, device="cuda")
+    pad[..., :dh] = to_device(w, inp.kv)
+    lay2 = B.cr_kv_layout(L, H, dh, B.CR_DTYPE_BF16, 2 * N * H * (dh + 16), N * H * (dh + 16),
+                          H * (dh + 16), dh + 16)
+    rep.repair(pad, w.chunk_offsets, w.request_chunks, emb, layout=lay2)
+    torch.cuda.synchronize()
+    got_tm = tm.float().cpu().numpy().transpose(0, 1, 2, 3, 4).reshape(N, -1)
+    got_pad = W.kv_layer_major_to_canonical(pad[..., :dh].float().cpu().numpy())
+    assert np.array_equal(got_tm, ref)
+    assert np.array_equal(got_pad, ref)
+    assert torch.all(pad[..., dh:] == 0)      # padding untouched

@@ -140,6 +140,18 @@ def test_unit_chunks_are_causal_sdpa():
     assert np.max(np.abs(got - _sdpa(q, k, v, True))) < 1e-13
 
 
+@pytest.mark.parametrize("lengths", [((3, 1, 4), (2, 3)), ((5,),), ((2, 0, 3),), ((1, 1, 1),)])
+def test_chunkwise_attention_equals_explicit_mask(lengths):
+    w = small_workload(lengths)
+    n = w.n_tokens
+    q, k, v = (_rs(s).standard_normal((n, 2, 4)) for s in (30, 31, 32))
+    c = O.token_chunk_ids(w.chunk_offsets)
+    r = O.token_request_ids(w.chunk_offsets, w.request_chunks)
+    ref = O.masked_attention(q, k, v, O.block_causal_allowed(c, r))
+    got = O.block_causal_attention(q, k, v, w.chunk_offsets, w.request_chunks)
+    assert np.max(np.abs(got - ref)) < 1e-13
+
+
 def test_attention_constant_values_pass_through():
     n = 7
     q, k = (_rs(s).standard_normal((n, 2, 4)) for s in (14, 15))
