@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the CacheRepair repair forward pass on one MI355X.
+
+A step is one ``cr_repair`` call over the whole packed batch of the workload
+(default: the Qwen2.5-3B-shaped request of 8 chunks x 512 tokens, repairer
+d_c = d_b = 1024, 8 blocks, 16 heads, FFN 4x), with the stale cache, token
+embeddings and prepared weights already resident in HBM.  Prints one JSON
+line: repaired doc tokens/s and ms per request, the roofline of the dominant
+kernel measured live with HIP events on the library's stream, and the fp64
+CPU oracle timed on a bounded sample on this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "repair latency ms + repaired doc tokens/s, 8×512-token chunks, Qwen2.5-3B KV"
+PEAK = {"bf16_tflops": 2500.0, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
+
+# kernel class (as reported by cr_profile_read) -> kernel function it launches
+FUNCTION_OF = {
+    "gemm_compress": "gemm_nt_kernel<EpiBias>", "gemm_token": "gemm_nt_kernel<EpiBias>",
+    "gemm_fuse": "gemm_nt_kernel<EpiBias>", "gemm_inject": "gemm_nt_kernel<EpiBias>",
+    "gemm_oproj": "gemm_nt_kernel<EpiBias>", "gemm_ffn1": "gemm_nt_kernel<EpiBias>",
+    "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKV>",
+    "gemm_expand": "gemm_nt_kernel<EpiExpand>", "attention": "attention_kernel",
+    "layernorm": "layernorm_kernel", "compress_segments": "compress_segments_kernel",
+    "schedule": "schedule_kernel", "rope_table": "rope_table_kernel",
+}
+
+
+def allowed_pairs(w):
+    """Query/key pairs the block-causal mask allows (per head)."""
+    pairs = 0
+    for req in w.chunk_lengths:
+        seen = 0
+        for L in req:
+            seen += L
+            pairs += L * seen
+    return pairs
+
+
+def algorithmic_work(w):
+    """Per-step algorithmic FLOPs and HBM bytes of every kernel class.
+
+    Weights are counted once per launch; attention counts only allowed
+    pairs (QK^T and PV, 2 FLOPs per MAC); the cache is read once by the
+    compression and read + written once by the expansion-add.
+    """
+    t, r = w.target, w.rep
+    N, D, S = w.n_tokens, t.d_kv, t.n_segments
+    E, dc, db, B, m = t.d_model, r.d_c, r.d_b, r.n_blocks, r.ffn_mult
+    kc = S * r.d_seg
+    es = 2 if w.dtype == "bf16" else 4
+    gemm = lambda n_out, k: (2.0 * N * n_out * k, es * (N * k + n_out * k + N * n_out))
+    work = {
+        "compress_segments": (2.0 * N * D * r.d_seg, es * (N * D + N * kc + S * r.d_seg * t.head_dim), 1),
+        "gemm_compress": (*gemm(dc, kc), 1),
+        "gemm_token": (*gemm(db, E), 1),
+        "gemm_fuse": (*gemm(db, dc + db), 1),
+        "gemm_inject": tuple(x * B for x in gemm(db, dc)) + (B,),
+        "gemm_qkv": tuple(x * B for x in gemm(3 * db, db)) + (B,),
+        "attention": (4.0 * allowed_pairs(w) * db * B, es * 4 * N * db * B, B),
+        "gemm_oproj": tuple(x * B for x in gemm(db, db)) + (B,),
+        "gemm_ffn1": tuple(x * B for x in gemm(m * db, db)) + (B,),
+        "gemm_ffn2": tuple(x * B for x in gemm(db, m * db)) + (B,),
+        "layernorm": (0.0, es * 2 * N * (dc + db * (2 * B + 1)), 2 + 2 * B),
+        "gemm_expand": (2.0 * N * db * D, es * (2 * N * D + D * db + N * db), 1),
+    }
+    return {k: {"flops": v[0], "bytes": v[1], "launches": v[2]} for k, v in work.items()}
+
+
+def bound_of(cls):
+    return "hbm" if cls in ("compress_segments", "layernorm") else "mfma"
+
+
+def time_oracle_sample(w, inp, max_chunks):
+    """fp64 oracle on the first max_chunks chunks of every request (a complete
+    sub-batch: earlier chunks never see later ones)."""
+    import numpy as np
+    import workloads as W
+    from oracle import repair
+    off, rc = w.chunk_offsets, w.request_chunks
+    idx, lens, reqs = [], [], [0]
+    for q in range(len(rc) - 1):
+        c1 = min(rc[q + 1], rc[q] + max_chunks)
+        for c in range(rc[q], c1):
+            idx.extend(range(off[c], off[c + 1]))
+            lens.append(off[c + 1] - off[c])
+        reqs.append(reqs[-1] + c1 - rc[q])
+    idx = np.array(idx)
+    X = W.kv_layer_major_to_canonical(inp.kv[:, :, idx])
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    t0 = time.perf_counter()
+    repair(X, inp.token_embeds[idx], offs, np.array(reqs), inp.weights, w.target.head_dim,
+           w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps)
+    dt = time.perf_counter() - t0
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(i.get("num_threads", 0) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    cores = threads or len(os.sched_getaffinity(0))
+    return {"value": len(idx) / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {max_chunks} chunk(s) of every request ({len(idx)} of "
+                      f"{w.n_tokens} tokens), full repairer, fp64 numpy/scipy",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen3b-8x512")
+    ap.add_argument("--oracle-chunks", type=int, default=4,
+                    help="chunks per request in the CPU oracle sample (0 = skip)")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time single calls after flushing the last-level cache")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs the repair of one request batch on one GPU; "
+              f"--gpus {args.gpus} is not supported (multi-GPU sharding is design-only).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2609_35139_amd import binding as B
+    from paper_2609_35139_amd.repairer import TORCH_DTYPE, Repairer, storage_dtype
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    w = W.workload(args.workload)
+    t, r = w.target, w.rep
+    print(f"[bench] generating {w.name} ({w.n_tokens} tokens)", file=sys.stderr, flush=True)
+    inp = W.make_inputs(w)
+    dt = storage_dtype(w.dtype)
+    dims = B.make_dims(t.d_model, r.d_seg, r.d_c, r.d_b, r.n_blocks, r.n_heads, r.ffn_mult,
+                       r.rope_theta, r.ln_eps)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        rep = Repairer(dims, t.n_layers, t.n_kv_heads, t.head_dim, dt, inp.weights,
+                       stream=stream)
+        kv = torch.from_numpy(inp.kv).to(TORCH_DTYPE[dt]).cuda()
+        emb = torch.from_numpy(inp.token_embeds).to(TORCH_DTYPE[dt]).cuda()
+        ws = rep.workspace(w.n_tokens)
+    stream.synchronize()
+    off, req = w.chunk_offsets, w.request_chunks
+
+    def step():
+        rep.repair(kv, off, req, emb, workspace=ws, stream=stream)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    stream.synchronize()
+
+    # ---- timed region: exactly K steps
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # ---- per-kernel HIP events recorded by the library on the same stream
+    work = algorithmic_work(w)
+    per_step_launches = sum(v["launches"] for v in work.values()) + 2
+    B.cr_profile_enable(per_step_launches * args.steps + 16)
+    for _ in range(args.steps):
+        step()
+    stats = B.cr_profile_read()
+    B.cr_profile_enable(0)
+    torch.cuda.synchronize()
+    kernels = []
+    for s in stats:
+        cls = s["name"]
+        avg_ms = s["total_ms"] / s["launches"]
+        entry = {"class": cls, "function": FUNCTION_OF.get(cls, cls), "launches_per_step":
+                 s["launches"] // args.steps, "avg_us": avg_ms * 1e3,
+                 "ms_per_step": s["total_ms"] / args.steps}
+        if cls in work:
+            wk = work[cls]
+            per_launch_fl = wk["flops"] / wk["launches"]
+            per_launch_by = wk["bytes"] / wk["launches"]
+            entry["tflops"] = per_launch_fl / (avg_ms * 1e-3) / 1e12
+            entry["gbs"] = per_launch_by / (avg_ms * 1e-3) / 1e9
+            if bound_of(cls) == "mfma":
+                entry["frac_mfma"] = entry["tflops"] / PEAK["bf16_tflops" if w.dtype == "bf16" else "f32_tflops"]
+            else:
+                entry["frac_hbm"] = entry["gbs"] / PEAK["hbm_gbs"]
+        kernels.append(entry)
+    # dominant kernel: the class (one kernel, one shape) with the most time per step
+    dom_entry = max((k for k in kernels if k["class"] in work), key=lambda k: k["ms_per_step"])
+    dom_cls = dom_entry["class"]
+    wk = work[dom_cls]
+    avg_launch_s = dom_entry["avg_us"] * 1e-6
+    mfma = bound_of(dom_cls) == "mfma"
+    if mfma:
+        achieved = wk["flops"] / wk["launches"] / avg_launch_s / 1e12
+        peak = PEAK["bf16_tflops" if w.dtype == "bf16" else "f32_tflops"]
+    else:
+        achieved = wk["bytes"] / wk["launches"] / avg_launch_s / 1e9
+        peak = PEAK["hbm_gbs"]
+    roofline = {"kernel": f"{dom_cls} ({dom_entry['function']})", "bound": "mfma" if mfma else "hbm",
+                "achieved": achieved, "peak": peak, "unit": "TFLOP/s" if mfma else "GB/s",
+                "frac": achieved / peak, "traffic": None, "avg_launch_us": avg_launch_s * 1e6,
+                "launches_per_step": wk["launches"],
+                "algorithmic_per_launch": (wk["flops"] if mfma else wk["bytes"]) / wk["launches"]}
+
+    cold = None
+    if args.cold:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        ts = []
+        for _ in range(min(args.steps, 20)):
+            with torch.cuda.stream(stream):
+                flush.zero_()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            step()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        cold = float(np.median(ts))
+
+    cpu = None
+    if args.oracle_chunks > 0:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = time_oracle_sample(w, inp, args.oracle_chunks)
+
+    total_flops = sum(v["flops"] for v in work.values())
+    out = {
+        "metric": METRIC, "value": w.n_tokens / (ms * 1e-3), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "ms_per_request": ms / w.n_requests,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded stale KV, embeddings and random-init repairer)",
+        "config": {"workload": w.name, "target": f"{t.name}-shaped KV: {t.n_layers} layers, "
+                   f"{t.n_kv_heads} KV heads, head_dim {t.head_dim}",
+                   "n_tokens": w.n_tokens, "n_chunks": w.n_chunks, "n_requests": w.n_requests,
+                   "repairer": f"d_seg={r.d_seg} d_c={r.d_c} d_b={r.d_b} blocks={r.n_blocks} "
+                               f"heads={r.n_heads} ffn={r.ffn_mult}x"},
+        "wall_s_timed": wall,
+        "step_tflops": total_flops / (ms * 1e-3) / 1e12,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "cold_ms_per_step": cold,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

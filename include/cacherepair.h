@@ -207,6 +207,26 @@ CR_API cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layo
                             int64_t n_tokens, const char* name,
                             uint64_t* offset_bytes, int64_t* row_stride);
 
+/*
+ * Per-launch timing (tracing aid, not needed for repair).  While enabled,
+ * cr_repair brackets every kernel launch with HIP events recorded on the
+ * call's own stream.  cr_profile_enable(max_launches) creates the events
+ * (host-side allocation happens here, never inside cr_repair);
+ * max_launches = 0 disables profiling and destroys them.  Launches beyond
+ * max_launches since the last reset are not timed.  cr_profile_read waits for
+ * the recorded events, then fills up to max_stats entries, one per kernel
+ * class in first-launch order, and resets the record.  This is process-wide
+ * state guarded by a mutex; profile one stream at a time.
+ */
+typedef struct {
+    char name[32];        /* kernel class, e.g. "attention", "gemm_ffn1" */
+    int32_t launches;
+    double total_ms;
+} cr_kernel_stat;
+
+CR_API cr_status cr_profile_enable(int32_t max_launches);
+CR_API cr_status cr_profile_read(cr_kernel_stat* stats, int32_t max_stats, int32_t* n_stats);
+
 #ifdef __cplusplus
 }
 #endif

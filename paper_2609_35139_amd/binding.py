@@ -29,7 +29,7 @@ STATUS = {
 }
 EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_bytes",
            "cr_prepare_weights", "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair",
-           "cr_workspace_view"]
+           "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]
 
 
 class CrError(RuntimeError):
@@ -49,6 +49,10 @@ class cr_dims(ctypes.Structure):
     _fields_ = [("d_model", c_int32), ("d_seg", c_int32), ("d_c", c_int32), ("d_b", c_int32),
                 ("n_blocks", c_int32), ("n_heads", c_int32), ("ffn_mult", c_int32),
                 ("rope_theta", c_float), ("ln_eps", c_float)]
+
+
+class cr_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", c_char * 32), ("launches", c_int32), ("total_ms", ctypes.c_double)]
 
 
 class cr_tensor_desc(ctypes.Structure):
@@ -85,8 +89,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                               c_uint64, c_void_p]
     lib.cr_workspace_view.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, c_char_p,
                                       P(c_uint64), P(c_int64)]
+    lib.cr_profile_enable.argtypes = [c_int32]
+    lib.cr_profile_read.argtypes = [P(cr_kernel_stat), c_int32, P(c_int32)]
     for name in ["cr_weights_layout", "cr_prepared_bytes", "cr_prepare_weights",
-                 "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_workspace_view"]:
+                 "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_workspace_view",
+                 "cr_profile_enable", "cr_profile_read"]:
         getattr(lib, name).restype = c_int32
     _lib = lib
     return lib
@@ -181,6 +188,19 @@ def cr_workspace_view(dims: cr_dims, layout: cr_kv_layout, n_tokens: int,
                                     name.encode(), ctypes.byref(off), ctypes.byref(ld)),
            "cr_workspace_view")
     return off.value, ld.value
+
+
+def cr_profile_enable(max_launches: int) -> None:
+    _check(load().cr_profile_enable(max_launches), "cr_profile_enable")
+
+
+def cr_profile_read() -> List[dict]:
+    lib = load()
+    n = c_int32(0)
+    table = (cr_kernel_stat * 64)()
+    _check(lib.cr_profile_read(table, 64, ctypes.byref(n)), "cr_profile_read")
+    return [{"name": table[i].name.decode(), "launches": table[i].launches,
+             "total_ms": table[i].total_ms} for i in range(n.value)]
 
 
 # ---------------------------------------------------------- conveniences

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -222,6 +223,37 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   return w;
 }
 
+// ------------------------------------------------------------- profiling
+struct Profiler {
+  std::mutex mu;
+  std::vector<hipEvent_t> ev;        // 2 per launch slot
+  std::vector<std::string> cls;      // class of each used slot
+  int used = 0;
+  bool on = false;
+};
+Profiler& prof() {
+  static Profiler p;
+  return p;
+}
+
+// Launch `f` on stream s, bracketed by events when profiling is enabled.
+template <typename F>
+hipError_t timed(const char* name, hipStream_t s, F&& f) {
+  Profiler& P = prof();
+  int slot = -1;
+  if (P.on) {
+    std::lock_guard<std::mutex> g(P.mu);
+    if (P.on && P.used < (int)P.ev.size() / 2) {
+      slot = P.used++;
+      P.cls.emplace_back(name);
+    }
+  }
+  if (slot >= 0) hipEventRecord(P.ev[2 * slot], s);
+  const hipError_t e = f();
+  if (slot >= 0) hipEventRecord(P.ev[2 * slot + 1], s);
+  return e;
+}
+
 #define CR_TRY(...)                                 \
   do {                                            \
     if ((__VA_ARGS__) != hipSuccess) return CR_ERR_LAUNCH; \
@@ -316,37 +348,54 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
                          l->n_kv_heads, l->head_dim};
   const float eps = d->ln_eps;
 
-  CR_TRY(cr::chunk_schedule(off, n_chunks, req, n_req, lo, hi, pos, s));
-  CR_TRY(cr::rope_table(rope, max_len, dhd, (double)d->rope_theta, s));
+  CR_TRY(timed("schedule", s, [&] {
+      return cr::chunk_schedule(off, n_chunks, req, n_req, lo, hi, pos, s); }));
+  CR_TRY(timed("rope_table", s, [&] {
+      return cr::rope_table(rope, max_len, dhd, (double)d->rope_theta, s); }));
   // StaleEncoder: per-segment projections, compression, LN_enc -> s = st[:, :d_c]
-  CR_TRY(cr::compress_segments<T>(kv, ks, l->n_layers, PT(P.w_seg), PF(P.b_seg), U, P.kc_pad,
-                                  d->d_seg, M, s));
-  CR_TRY(cr::gemm_bias<T>(U, P.kc_pad, PT(P.w_cmp), P.kc_pad, M, dc, (int)P.kc_pad, st, ldst,
-                          PF(P.b_cmp), nullptr, 0, false, s));
-  CR_TRY(cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s));
+  CR_TRY(timed("compress_segments", s, [&] {
+      return cr::compress_segments<T>(kv, ks, l->n_layers, PT(P.w_seg), PF(P.b_seg), U, P.kc_pad,
+                                  d->d_seg, M, s); }));
+  CR_TRY(timed("gemm_compress", s, [&] {
+      return cr::gemm_bias<T>(U, P.kc_pad, PT(P.w_cmp), P.kc_pad, M, dc, (int)P.kc_pad, st, ldst,
+                          PF(P.b_cmp), nullptr, 0, false, s); }));
+  CR_TRY(timed("layernorm", s, [&] {
+      return cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s); }));
   // token projection -> st[:, d_c:], fusion -> h^0
-  CR_TRY(cr::gemm_bias<T>(emb, E, PT(P.w_tok), E, M, db, E, st + dc, ldst, PF(P.b_tok), nullptr,
-                          0, false, s));
-  CR_TRY(cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
-                          nullptr, 0, false, s));
+  CR_TRY(timed("gemm_token", s, [&] {
+      return cr::gemm_bias<T>(emb, E, PT(P.w_tok), E, M, db, E, st + dc, ldst, PF(P.b_tok), nullptr,
+                          0, false, s); }));
+  CR_TRY(timed("gemm_fuse", s, [&] {
+      return cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
+                          nullptr, 0, false, s); }));
   for (int b = 0; b < d->n_blocks; ++b) {
     const BlockP& B = P.blk[b];
-    CR_TRY(cr::gemm_bias<T>(st, ldst, PT(B.w_inj), dc, M, db, dc, h, db, PF(B.b_inj), h, db,
-                            false, s));
-    CR_TRY(cr::layernorm<T>(h, db, a, db, PF(B.ln1_g), PF(B.ln1_b), M, db, eps, s));
-    CR_TRY(cr::gemm_qkv<T>(a, db, PT(B.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(B.b_qkv),
-                           pos, rope, s));
-    CR_TRY(cr::attention<T>(q, k, vt, o, M, db, nh, dhd, W.n_pad, lo, hi, s));
-    CR_TRY(cr::gemm_bias<T>(o, db, PT(B.w_o), db, M, db, db, h, db, PF(B.b_o), h, db, false, s));
-    CR_TRY(cr::layernorm<T>(h, db, a, db, PF(B.ln2_g), PF(B.ln2_b), M, db, eps, s));
-    CR_TRY(cr::gemm_bias<T>(a, db, PT(B.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
-                            PF(B.b_ff1), nullptr, 0, true, s));
-    CR_TRY(cr::gemm_bias<T>(f, (int64_t)r * db, PT(B.w_ff2), (int64_t)r * db, M, db, r * db, h,
-                            db, PF(B.b_ff2), h, db, false, s));
+    CR_TRY(timed("gemm_inject", s, [&] {
+        return cr::gemm_bias<T>(st, ldst, PT(B.w_inj), dc, M, db, dc, h, db, PF(B.b_inj), h, db,
+                            false, s); }));
+    CR_TRY(timed("layernorm", s, [&] {
+        return cr::layernorm<T>(h, db, a, db, PF(B.ln1_g), PF(B.ln1_b), M, db, eps, s); }));
+    CR_TRY(timed("gemm_qkv", s, [&] {
+        return cr::gemm_qkv<T>(a, db, PT(B.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(B.b_qkv),
+                           pos, rope, s); }));
+    CR_TRY(timed("attention", s, [&] {
+        return cr::attention<T>(q, k, vt, o, M, db, nh, dhd, W.n_pad, lo, hi, s); }));
+    CR_TRY(timed("gemm_oproj", s, [&] {
+        return cr::gemm_bias<T>(o, db, PT(B.w_o), db, M, db, db, h, db, PF(B.b_o), h, db, false, s); }));
+    CR_TRY(timed("layernorm", s, [&] {
+        return cr::layernorm<T>(h, db, a, db, PF(B.ln2_g), PF(B.ln2_b), M, db, eps, s); }));
+    CR_TRY(timed("gemm_ffn1", s, [&] {
+        return cr::gemm_bias<T>(a, db, PT(B.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
+                            PF(B.b_ff1), nullptr, 0, true, s); }));
+    CR_TRY(timed("gemm_ffn2", s, [&] {
+        return cr::gemm_bias<T>(f, (int64_t)r * db, PT(B.w_ff2), (int64_t)r * db, M, db, r * db, h,
+                            db, PF(B.b_ff2), h, db, false, s); }));
   }
-  CR_TRY(cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s));
-  CR_TRY(cr::gemm_expand<T>(a, db, PT(P.w_out), M, D, db, kv, ks, PF(P.b_out),
-                            PF(P.sigma_delta), s));
+  CR_TRY(timed("layernorm", s, [&] {
+      return cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s); }));
+  CR_TRY(timed("gemm_expand", s, [&] {
+      return cr::gemm_expand<T>(a, db, PT(P.w_out), M, D, db, kv, ks, PF(P.b_out),
+                            PF(P.sigma_delta), s); }));
   return CR_OK;
 }
 
@@ -506,6 +555,53 @@ cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_o
                             request_chunks, n_requests, static_cast<const float*>(token_embeds),
                             dims, static_cast<const char*>(prepared),
                             static_cast<char*>(workspace), N, max_len, s);
+}
+
+cr_status cr_profile_enable(int32_t max_launches) {
+  if (max_launches < 0) return CR_ERR_DIMS;
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  for (hipEvent_t e : P.ev) hipEventDestroy(e);
+  P.ev.clear();
+  P.cls.clear();
+  P.used = 0;
+  P.on = false;
+  if (max_launches == 0) return CR_OK;
+  P.ev.resize(2 * (size_t)max_launches);
+  for (hipEvent_t& e : P.ev)
+    if (hipEventCreate(&e) != hipSuccess) return CR_ERR_DEVICE;
+  P.on = true;
+  return CR_OK;
+}
+
+cr_status cr_profile_read(cr_kernel_stat* stats, int32_t max_stats, int32_t* n_stats) {
+  if (!n_stats) return CR_ERR_NULL;
+  Profiler& P = prof();
+  std::lock_guard<std::mutex> g(P.mu);
+  std::vector<std::string> names;
+  std::vector<int> launches;
+  std::vector<double> total;
+  for (int i = 0; i < P.used; ++i) {
+    if (hipEventSynchronize(P.ev[2 * i + 1]) != hipSuccess) return CR_ERR_LAUNCH;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, P.ev[2 * i], P.ev[2 * i + 1]) != hipSuccess) return CR_ERR_LAUNCH;
+    size_t k = std::find(names.begin(), names.end(), P.cls[i]) - names.begin();
+    if (k == names.size()) { names.push_back(P.cls[i]); launches.push_back(0); total.push_back(0); }
+    launches[k] += 1;
+    total[k] += ms;
+  }
+  P.used = 0;
+  P.cls.clear();
+  *n_stats = (int32_t)names.size();
+  if (!stats) return CR_OK;
+  if (max_stats < (int32_t)names.size()) return CR_ERR_CAPACITY;
+  for (size_t k = 0; k < names.size(); ++k) {
+    std::memset(&stats[k], 0, sizeof(cr_kernel_stat));
+    std::strncpy(stats[k].name, names[k].c_str(), sizeof(stats[k].name) - 1);
+    stats[k].launches = launches[k];
+    stats[k].total_ms = total[k];
+  }
+  return CR_OK;
 }
 
 }  // extern "C"

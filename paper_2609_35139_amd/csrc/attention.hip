@@ -16,9 +16,12 @@
 // sub-tile are fed to the MFMA in an order (bits 2 and 3 of the row index
 // swapped) that makes the score accumulator registers coincide with the B
 // operand of the P V product, so probabilities never leave registers.
-// V arrives transposed (vt[head][d][token]) from the QKV epilogue and is
-// staged in LDS as [d][key], which turns the A operand of O^T = V^T P^T into
-// contiguous 16-byte reads.  K/V tiles are double-buffered through LDS.
+// V arrives transposed (vt[head][d][token]) from the QKV epilogue, so the
+// A operand of O^T = V^T P^T is a contiguous 16-byte read.  K and V^T tiles
+// stream through a four-stage LDS ring filled by global_load_lds.  The
+// softmax reference max is only raised when a row max grows by more than
+// 2^8 (in exp2 units), which keeps probabilities <= 256 and skips almost
+// every rescale of the output accumulators.
 #include <climits>
 
 #include "launch.h"
@@ -27,11 +30,14 @@ namespace cr {
 
 template <typename T, int D>
 struct AttnCfg {
-  static constexpr int BQ = 128, BKV = 64;
+  static constexpr int BQ = 128, BKV = 64, STAGES = 4;
   static constexpr int VEC = 16 / (int)sizeof(T);
-  static constexpr int LDK = D + VEC;      // K tile row (elements)
-  static constexpr int LDV = BKV + VEC;    // V^T tile row (elements)
-  static constexpr int KVEC = BKV * D / VEC / 256;  // 16-byte loads per thread per tile
+  static constexpr int RBK = D * (int)sizeof(T);      // K tile row bytes
+  static constexpr int RBV = BKV * (int)sizeof(T);    // V^T tile row bytes
+  static constexpr int K_BYTES = BKV * RBK, V_BYTES = D * RBV;
+  static constexpr int K_ROUNDS = K_BYTES / 4096, V_ROUNDS = V_BYTES / 4096;
+  static constexpr int OPS = K_ROUNDS + V_ROUNDS;     // DMA ops per thread per tile
+  static constexpr int STAGE_BYTES = K_BYTES + V_BYTES;
 };
 
 // A-operand row r of a 32-key sub-tile reads key swap_bits23(r).
@@ -53,11 +59,12 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
   using C = AttnCfg<T, D>;
   using MM = Mma32<T>;
   using frag = typename MM::frag;
+  using SK = Swz<C::RBK>;
+  using SV = Swz<C::RBV>;
   constexpr int KPL = MM::KPL, KSTEP = MM::KSTEP;
   constexpr int QF = D / KSTEP;          // Q fragments per lane
   constexpr int DT = D / 32;             // 32-row tiles of O^T
-  __shared__ __align__(16) T Ks[2][C::BKV * C::LDK];
-  __shared__ __align__(16) T Vs[2][D * C::LDV];
+  __shared__ __align__(1024) char ring[C::STAGES * C::STAGE_BYTES];
   __shared__ int red[2][4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -92,92 +99,112 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
     else qf[s] = frag{};
   }
 
-  const T* kbase = Kg + head * D;
-  const T* vbase = Vt + (int64_t)head * D * n_pad;
-  uint4 rk[C::KVEC], rv[C::KVEC];
-  auto gload = [&](int k0) {
+  // DMA sources (per lane, for the tile starting at key kb): K rows are keys
+  // (clamped to N-1 past the end: such keys are always masked), V^T rows are d.
+  const char* ksrc[C::K_ROUNDS];
+  const char* vsrc[C::V_ROUNDS];
+  int krow0[C::K_ROUNDS];
 #pragma unroll
-    for (int p = 0; p < C::KVEC; ++p) {
-      const int v = tid + p * 256;
-      const int kr = v / (D / C::VEC), kc = (v % (D / C::VEC)) * C::VEC;
-      const int key = k0 + kr;
-      rk[p] = key < N ? *reinterpret_cast<const uint4*>(kbase + (int64_t)key * d_b + kc)
-                      : make_uint4(0, 0, 0, 0);
-      const int vr = v / (C::BKV / C::VEC), vc = (v % (C::BKV / C::VEC)) * C::VEC;
-      rv[p] = *reinterpret_cast<const uint4*>(vbase + (int64_t)vr * n_pad + k0 + vc);
-    }
-  };
-  auto lstore = [&](int buf) {
+  for (int r = 0; r < C::K_ROUNDS; ++r) {
+    const int row = (r * 4 + wave) * SK::RPW + lane / SK::CPR;
+    krow0[r] = row;
+    const int chunk = SK::slot(row, lane % SK::CPR);
+    ksrc[r] = reinterpret_cast<const char*>(Kg + head * D) + chunk * 16;
+  }
 #pragma unroll
-    for (int p = 0; p < C::KVEC; ++p) {
-      const int v = tid + p * 256;
-      const int kr = v / (D / C::VEC), kc = (v % (D / C::VEC)) * C::VEC;
-      *reinterpret_cast<uint4*>(&Ks[buf][kr * C::LDK + kc]) = rk[p];
-      const int vr = v / (C::BKV / C::VEC), vc = (v % (C::BKV / C::VEC)) * C::VEC;
-      *reinterpret_cast<uint4*>(&Vs[buf][vr * C::LDV + vc]) = rv[p];
-    }
-  };
+  for (int r = 0; r < C::V_ROUNDS; ++r) {
+    const int row = (r * 4 + wave) * SV::RPW + lane / SV::CPR;
+    const int chunk = SV::slot(row, lane % SV::CPR);
+    vsrc[r] = reinterpret_cast<const char*>(Vt + ((int64_t)head * D + row) * n_pad + kb) + chunk * 16;
+  }
+  const int64_t krow_bytes = (int64_t)d_b * sizeof(T);
 
   f32x16 oacc[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) oacc[d] = f32x16{};
-  float m = -INFINITY, lsum = 0.f;
+  float m_ref = -INFINITY, lsum = 0.f;
   const int krow = swap_bits23(ql);
 
-  if (ntiles > 0) {
-    gload(kb);
-    lstore(0);
-  }
-  __syncthreads();
+#define CR_ATTN_ISSUE(TILE, STAGE)                                                         \
+  do {                                                                                     \
+    char* base_ = ring + (STAGE) * C::STAGE_BYTES;                                         \
+    const int k0_ = kb + (TILE) * C::BKV;                                                  \
+    _Pragma("unroll") for (int r = 0; r < C::K_ROUNDS; ++r) {                              \
+      const int key_ = min(k0_ + krow0[r], N - 1);                                         \
+      dma16(ksrc[r] + key_ * krow_bytes, base_ + (r * 4 + wave) * 1024);                   \
+    }                                                                                      \
+    _Pragma("unroll") for (int r = 0; r < C::V_ROUNDS; ++r)                                \
+      dma16(vsrc[r] + (int64_t)(TILE) * C::BKV * sizeof(T),                                \
+            base_ + C::K_BYTES + (r * 4 + wave) * 1024);                                   \
+  } while (0)
+
+#pragma unroll
+  for (int st = 0; st < C::STAGES - 1; ++st)
+    if (st < ntiles) CR_ATTN_ISSUE(st, st);
+
   for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
+    const int ahead = min(C::STAGES - 2, ntiles - 1 - t);
+    if (ahead >= 2) wait_vmcnt<2 * C::OPS>();
+    else if (ahead == 1) wait_vmcnt<C::OPS>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (t + C::STAGES - 1 < ntiles) CR_ATTN_ISSUE(t + C::STAGES - 1, (t + C::STAGES - 1) % C::STAGES);
+
+    const char* ks_ = ring + (t % C::STAGES) * C::STAGE_BYTES;
+    const char* vs_ = ks_ + C::K_BYTES;
     const int k0 = kb + t * C::BKV;
-    if (t + 1 < ntiles) gload(k0 + C::BKV);
 
     // S^T for two 32-key sub-tiles
     f32x16 s[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       s[rt] = f32x16{};
+      const int row = rt * 32 + krow;
 #pragma unroll
       for (int ks = 0; ks < QF; ++ks) {
-        const frag a = load_frag<T, frag>(&Ks[cur][(rt * 32 + krow) * C::LDK + ks * KSTEP + g * KPL]);
+        const int k = ks * KSTEP + g * KPL;
+        const frag a = *reinterpret_cast<const frag*>(ks_ + SK::offset(row, k / C::VEC) +
+                                                      (k % C::VEC) * (int)sizeof(T));
         s[rt] = MM::mma(a, qf[ks], s[rt]);
       }
     }
     const bool need_mask = !(k0 >= wmax_lo && k0 + C::BKV <= wmin_hi);
+    if (need_mask) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = k0 + rt * 32 + score_key(g, i);
+          if (key < mlo || key >= mhi) s[rt][i] = -INFINITY;
+        }
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float v = s[rt][i] * scale_log2;
-        if (need_mask) {
-          const int key = k0 + rt * 32 + score_key(g, i);
-          if (key < mlo || key >= mhi) v = -INFINITY;
-        }
-        s[rt][i] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-    const float m_new = fmaxf(m, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m - m_use);
-    m = m_new;
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rt][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * scale_log2;
+    if (__any(mx > m_ref + 8.0f)) {
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_ref - m_new);
+      m_ref = m_new;
+      lsum *= alpha;
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
+    }
+    const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
     float psum = 0.f;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(s[rt][i] - m_use);
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rt][i], scale_log2, -m_use));
         s[rt][i] = p;
         psum += p;
       }
-    lsum = lsum * alpha + psum;
-#pragma unroll
-    for (int d = 0; d < DT; ++d)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
+    lsum += psum;
 
     // O^T += V^T P^T
 #pragma unroll
@@ -191,14 +218,13 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
         const int kofs = rt * 32 + score_key(g, s2 * KPL);
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          const frag a = load_frag<T, frag>(&Vs[cur][(d * 32 + ql) * C::LDV + kofs]);
+          const frag a = *reinterpret_cast<const frag*>(
+              vs_ + SV::offset(d * 32 + ql, kofs / C::VEC) + (kofs % C::VEC) * (int)sizeof(T));
           oacc[d] = MM::mma(a, b, oacc[d]);
         }
       }
-
-    if (t + 1 < ntiles) lstore(cur ^ 1);
-    __syncthreads();
   }
+#undef CR_ATTN_ISSUE
 
   if (!qvalid) return;
   const float total = lsum + __shfl_xor(lsum, 32, WAVE);

@@ -118,6 +118,40 @@ __device__ __forceinline__ bf16x8 pack_frag(const float* f, bf16x8*) {
 }
 __device__ __forceinline__ float pack_frag(const float* f, float*) { return f[0]; }
 
+// ------------------------------------------------- direct global -> LDS
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
+
+// One 16-byte global -> LDS transfer per lane (global_load_lds_dwordx4): a
+// wave writes 64 consecutive 16-byte slots starting at `lds_wave_base`
+// (wave-uniform), lane l filling slot l.  Completion is tracked by vmcnt.
+__device__ __forceinline__ void dma16(const void* gsrc, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((glb_void*)gsrc, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Tiles staged in LDS as rows of RB bytes (64, 128 or 256) made of 16-byte
+// chunks.  Chunk c of row r lives in slot c ^ ((r / (256 / RB)) % (RB / 16)):
+// the rows read together by a 16-lane group of a fragment load then start
+// in distinct banks.  A wave's 1 KB DMA round fills 1024 / RB whole rows.
+template <int RB>
+struct Swz {
+  static constexpr int CPR = RB / 16;          // chunks per row
+  static constexpr int RPW = 1024 / RB;        // rows per wave DMA round
+  __device__ __forceinline__ static int slot(int row, int chunk) {
+    return chunk ^ ((row / (256 / RB)) % CPR);
+  }
+  __device__ __forceinline__ static int offset(int row, int chunk) {
+    return row * RB + (slot(row, chunk) << 4);
+  }
+};
+__device__ __forceinline__ int swz128(int row) { return (row >> 1) & 7; }
+
 // --------------------------------------------------------- reductions
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

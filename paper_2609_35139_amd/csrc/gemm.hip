@@ -1,67 +1,99 @@
 // Tiled MFMA GEMM for the repair network's dense projections (gfx950).
 //
 // C[M][N] = A[M][K] * B[N][K]^T with both operands K-contiguous (activations
-// row-major, weights prepared as [out][in]).  A 256-thread workgroup owns a
-// 128x128 output tile; each of its four waves owns a 64x64 quadrant computed
-// with 16x16 MFMA atoms (bf16: 16x16x32, fp32: 16x16x4).  K advances in
-// 128-byte slabs that are double-buffered through LDS: global loads for slab
-// k+1 are in flight while slab k is multiplied.  The fp32 accumulators are
-// then staged through LDS so that every epilogue reads and writes whole
-// 16-byte row segments (bias, GELU, residual add, RoPE, transposed V, and the
+// row-major, weights prepared as [out][in]).  A 256-thread workgroup owns an
+// output tile split in four wave quadrants computed with 32x32 MFMA atoms.
+// K advances in slabs of 128 bytes per row, fetched straight from global
+// memory into an LDS ring with global_load_lds (no register staging); rows
+// are XOR-swizzled in LDS so fragment reads are conflict-free.  The fp32 accumulators are then
+// staged through LDS so that every epilogue reads and writes whole 16-byte
+// row segments (bias, GELU, residual add, RoPE, transposed V, and the
 // strided in-place add into the KV cache).
 #include "launch.h"
 
 namespace cr {
 
-template <typename T>
+// Tile geometry: a 2x2 grid of waves, each owning TM x TN MFMA atoms of
+// 32x32 (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32; on
+// gfx950 the 32x32 atoms sustain several times the rate of the 16x16 ones),
+// so the workgroup tile is (64*TM) x (64*TN).  K advances in slabs of one
+// 128-byte row per tile row; STAGES slabs live in the LDS ring.
+template <typename T, int TM_, int TN_, int STAGES_>
 struct GemmTile {
-  static constexpr int BM = 128, BN = 128;
-  static constexpr int BK = 128 / (int)sizeof(T);   // 64 bf16 / 32 fp32
-  static constexpr int VEC = 16 / (int)sizeof(T);   // elements per 16-byte load
-  static constexpr int LDK = BK + VEC;              // padded LDS row (elements)
-  static constexpr int TPR = BK / VEC;              // threads per tile row
-  static constexpr int RPP = 256 / TPR;             // rows per load pass
-  static constexpr int PASSES = BM / RPP;
-  static constexpr int WM = 64, WN = 64;
-  static constexpr int TM = WM / 16, TN = WN / 16;
-  static constexpr int LDC = BN + 4;                // fp32 staging row
-  static constexpr size_t LDS_MAIN = 2ull * (BM + BN) * LDK * sizeof(T);
+  static constexpr int TM = TM_, TN = TN_, STAGES = STAGES_;
+  static constexpr int NW = 4, NT = 256;
+  static constexpr int WM = 32 * TM, WN = 32 * TN;
+  static constexpr int BM = 2 * WM, BN = 2 * WN;
+  static constexpr int BK = 128 / (int)sizeof(T);   // elements per 128-byte row
+  static constexpr int VEC = 16 / (int)sizeof(T);   // elements per 16-byte chunk
+  static constexpr int A_ROUNDS = BM * 8 / NT;      // 16-byte DMA ops per thread per slab
+  static constexpr int B_ROUNDS = BN * 8 / NT;
+  static constexpr int OPS = A_ROUNDS + B_ROUNDS;
+  static constexpr int STAGE_BYTES = (BM + BN) * 128;
+  static constexpr int HC = BN / 2;                 // epilogue handles one column half at a time
+  static constexpr int LDC = HC + 4;                // fp32 staging row
+  static constexpr size_t LDS_MAIN = (size_t)STAGES * STAGE_BYTES;
   static constexpr size_t LDS_C = (size_t)BM * LDC * sizeof(float);
   static constexpr size_t LDS = LDS_MAIN > LDS_C ? LDS_MAIN : LDS_C;
+  static_assert(OPS * (STAGES - 2) <= 63, "vmcnt range");
 };
 
-// Visit the staged tile in 8-column row segments that fall inside [M) x [N).
-template <typename T, typename F>
-__device__ __forceinline__ void for_each_row8(int m0, int n0, int M, int N, F&& f) {
-  using G = GemmTile<T>;
-  constexpr int SEG = G::BN / 8;
-  for (int idx = threadIdx.x; idx < G::BM * SEG; idx += 256) {
-    const int r = idx / SEG, c = (idx % SEG) * 8;
-    const int gm = m0 + r, gn = n0 + c;
-    if (gm < M && gn < N) f(r, c, gm, gn);
-  }
+// Epilogues receive a staged block Cs[ROWS][LDC] (fp32) whose element (r, c)
+// is output (m0 + r, n0 + c).  Each thread owns one 8-column segment and a
+// strided set of rows, so per-column vectors (bias, sigma) are loaded once
+// and every global load of the segment's rows is issued before any of them
+// is needed.
+template <int ROWS, int COLS>
+struct SegMap {
+  static constexpr int SEG = COLS / 8;            // segments per row
+  static constexpr int RSTEP = 256 / SEG;         // rows between a thread's passes
+  static constexpr int PASSES = ROWS / RSTEP;
+  static_assert(256 % SEG == 0 && ROWS % RSTEP == 0, "segment map");
+  __device__ static int col() { return (threadIdx.x % SEG) * 8; }
+  __device__ static int row(int p) { return threadIdx.x / SEG + p * RSTEP; }
+};
+
+__device__ __forceinline__ void load8f(const float* p, float* v) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
 template <typename T>
 struct EpiBias {
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; int gelu;
-  __device__ void operator()(const float* Cs, int m0, int n0, int M, int N) const {
-    using G = GemmTile<T>;
-    for_each_row8<T>(m0, n0, M, N, [&](int r, int c, int gm, int gn) {
+  template <int ROWS, int COLS, int LDC>
+  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS>;
+    const int c = S::col(), gn = n0 + c;
+    if (gn >= N) return;
+    float b[8];
+    load8f(bias + gn, b);
+    Vec8<T> rv[S::PASSES];
+    if (resid) {
+#pragma unroll
+      for (int p = 0; p < S::PASSES; ++p) {
+        const int gm = m0 + S::row(p);
+        if (gm < M) rv[p].load(resid + (int64_t)gm * ldr + gn);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < S::PASSES; ++p) {
+      const int r = S::row(p), gm = m0 + r;
+      if (gm >= M) continue;
       float v[8];
+      load8f(Cs + r * LDC + c, v);
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        v[k] = Cs[r * G::LDC + c + k] + bias[gn + k];
+        v[k] += b[k];
         if (gelu) v[k] = gelu_erf(v[k]);
       }
       if (resid) {
-        Vec8<T> rv; rv.load(resid + (int64_t)gm * ldr + gn);
-        float rf[8]; rv.to_float(rf);
+        float rf[8]; rv[p].to_float(rf);
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = rf[k] + v[k];
       }
       Vec8<T> o; o.from_float(v); o.store(out + (int64_t)gm * ldo + gn);
-    });
+    }
   }
 };
 
@@ -69,34 +101,53 @@ template <typename T>
 struct EpiQKV {
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
-  __device__ void operator()(const float* Cs, int m0, int n0, int M, int N) const {
-    using G = GemmTile<T>;
+  template <int ROWS, int COLS, int LDC>
+  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
     if (n0 < 2 * d_b) {
       // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
+      // The block is head-aligned and never straddles Q/K (d_b % COLS == 0).
+      using S = SegMap<ROWS, COLS>;
       T* dst = n0 < d_b ? q : k;
       const int cbase = n0 < d_b ? n0 : n0 - d_b;
       const int half = d_head / 2;
-      for_each_row8<T>(m0, n0, M, N, [&](int r, int c, int gm, int gn) {
-        const int hc = c % d_head;  // n0 is a multiple of d_head
-        const bool first = hc < half;
-        const int pc = first ? c + half : c - half;
-        const int fi = first ? hc : hc - half;
-        const float2* cs = rope + (int64_t)pos[gm] * half + fi;
-        float v[8];
+      const int c = S::col(), gn = n0 + c;
+      const int hc = c % d_head;
+      const bool first = hc < half;
+      const int pc = first ? c + half : c - half;
+      const int fi = first ? hc : hc - half;
+      float bx[8], by[8];
+      load8f(bias + gn, bx);
+      load8f(bias + n0 + pc, by);
+      int pp[S::PASSES];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = Cs[r * G::LDC + c + e] + bias[gn + e];
-          const float y = Cs[r * G::LDC + pc + e] + bias[gn - c + pc + e];
-          const float2 t = cs[e];
-          v[e] = first ? x * t.x - y * t.y : x * t.x + y * t.y;
+      for (int p = 0; p < S::PASSES; ++p) {
+        const int gm = m0 + S::row(p);
+        pp[p] = gm < M ? pos[gm] : 0;
+      }
+#pragma unroll
+      for (int p = 0; p < S::PASSES; ++p) {
+        const int r = S::row(p), gm = m0 + r;
+        if (gm >= M) continue;
+        const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)pp[p] * half + fi);
+        float x[8], y[8], v[8];
+        load8f(Cs + r * LDC + c, x);
+        load8f(Cs + r * LDC + pc, y);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float4 t = cs4[e];   // (cos, sin) of pairs 2e and 2e+1
+          const float c0 = t.x, s0 = t.y, c1 = t.z, s1 = t.w;
+          const float x0 = x[2 * e] + bx[2 * e], y0 = y[2 * e] + by[2 * e];
+          const float x1 = x[2 * e + 1] + bx[2 * e + 1], y1 = y[2 * e + 1] + by[2 * e + 1];
+          v[2 * e] = first ? x0 * c0 - y0 * s0 : x0 * c0 + y0 * s0;
+          v[2 * e + 1] = first ? x1 * c1 - y1 * s1 : x1 * c1 + y1 * s1;
         }
         Vec8<T> o; o.from_float(v); o.store(dst + (int64_t)gm * d_b + cbase + c);
-      });
+      }
     } else {
       // V: write transposed, vt[head][d][token], 8 tokens per store.  Rows
-      // in [M, n_pad) hold bias-only values, keeping the padding finite.
-      constexpr int RSEG = G::BM / 8;
-      for (int idx = threadIdx.x; idx < G::BN * RSEG; idx += 256) {
+      // in [M, n_pad) hold values computed from clamped rows: finite padding.
+      constexpr int RSEG = ROWS / 8;
+      for (int idx = threadIdx.x; idx < COLS * RSEG; idx += 256) {
         const int c = idx / RSEG, r = (idx % RSEG) * 8;
         const int gn = n0 + c, gm = m0 + r;
         if (gn >= N || gm + 8 > n_pad) continue;
@@ -104,7 +155,7 @@ struct EpiQKV {
         const float bb = bias[gn];
         float v[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * G::LDC + c] + bb;
+        for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + c] + bb;
         Vec8<T> o; o.from_float(v);
         o.store(vt + (int64_t)vc * n_pad + gm);
       }
@@ -115,116 +166,171 @@ struct EpiQKV {
 template <typename T>
 struct EpiExpand {
   T* kv; KvStrides ks; const float* bias; const float* sigma;
-  __device__ void operator()(const float* Cs, int m0, int n0, int M, int N) const {
-    using G = GemmTile<T>;
-    for_each_row8<T>(m0, n0, M, N, [&](int r, int c, int gm, int gn) {
-      // coordinate j = ((l*2 + kv)*H + h)*d_h + i
-      const int i = gn % ks.head_dim;
-      const int seg = gn / ks.head_dim;
-      const int h = seg % ks.n_kv_heads;
-      const int lk = seg / ks.n_kv_heads;
-      T* p = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
-             (int64_t)gm * ks.token + (int64_t)h * ks.head + i;
-      Vec8<T> x; x.load(p);
-      float f[8]; x.to_float(f);
+  template <int ROWS, int COLS, int LDC>
+  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS>;
+    const int c = S::col(), gn = n0 + c;
+    if (gn >= N) return;
+    // coordinate j = ((l*2 + kv)*H + h)*d_h + i; 8 | d_h keeps a segment in one head
+    const int i = gn % ks.head_dim;
+    const int seg = gn / ks.head_dim;
+    const int h = seg % ks.n_kv_heads;
+    const int lk = seg / ks.n_kv_heads;
+    T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
+              (int64_t)h * ks.head + i;
+    float b[8], sg[8];
+    load8f(bias + gn, b);
+    load8f(sigma + gn, sg);
+    Vec8<T> x[S::PASSES];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = f[e] + sigma[gn + e] * (Cs[r * G::LDC + c + e] + bias[gn + e]);
-      x.from_float(f); x.store(p);
-    });
+    for (int p = 0; p < S::PASSES; ++p) {
+      const int gm = m0 + S::row(p);
+      if (gm < M) x[p].load(base + (int64_t)gm * ks.token);
+    }
+#pragma unroll
+    for (int p = 0; p < S::PASSES; ++p) {
+      const int r = S::row(p), gm = m0 + r;
+      if (gm >= M) continue;
+      float a[8], f[8];
+      load8f(Cs + r * LDC + c, a);
+      x[p].to_float(f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = f[e] + sg[e] * (a[e] + b[e]);
+      x[p].from_float(f);
+      x[p].store(base + (int64_t)gm * ks.token);
+    }
   }
 };
 
-template <typename T, typename Epi>
+// Wait until slab kt of the ring has landed: `ahead` later slabs may still
+// be in flight (OPS DMA operations each).
+template <int OPS, int MAXA>
+__device__ __forceinline__ void wait_slab(int ahead) {
+  if constexpr (MAXA >= 3) { if (ahead >= 3) { wait_vmcnt<3 * OPS>(); return; } }
+  if constexpr (MAXA >= 2) { if (ahead >= 2) { wait_vmcnt<2 * OPS>(); return; } }
+  if constexpr (MAXA >= 1) { if (ahead >= 1) { wait_vmcnt<OPS>(); return; } }
+  wait_vmcnt<0>();
+}
+
+template <typename T, typename G, typename Epi>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, int64_t lda,
                                                       const T* __restrict__ B, int64_t ldb,
                                                       int M, int N, int K, Epi epi) {
-  using G = GemmTile<T>;
-  using MM = Mma16<T>;
+  using MM = Mma32<T>;
   using frag = typename MM::frag;
-  __shared__ __align__(16) char smem[G::LDS];
-  T* As = reinterpret_cast<T*>(smem);
-  T* Bs = As + 2 * G::BM * G::LDK;
+  __shared__ __align__(1024) char smem[G::LDS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.y * G::BM, n0 = blockIdx.x * G::BN;
   const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
-  const int lr = tid / G::TPR, lc = (tid % G::TPR) * G::VEC;
 
-  uint4 ra[G::PASSES], rb[G::PASSES];
-  auto gload = [&](int k0) {
+  // DMA sources: in round r a wave fills 1 KB = rows (r*NW + wave)*8 + [0, 8)
+  // of the tile; lane l reads the chunk that lands in slot (l & 7) of its row.
+  // Rows past M / N are clamped to the last row: they only feed outputs that
+  // the epilogue discards.
+  const char* asrc[G::A_ROUNDS];
+  const char* bsrc[G::B_ROUNDS];
 #pragma unroll
-    for (int p = 0; p < G::PASSES; ++p) {
-      const int row = lr + p * G::RPP;
-      const int gm = m0 + row, gn = n0 + row;
-      ra[p] = gm < M ? *reinterpret_cast<const uint4*>(A + (int64_t)gm * lda + k0 + lc)
-                     : make_uint4(0, 0, 0, 0);
-      rb[p] = gn < N ? *reinterpret_cast<const uint4*>(B + (int64_t)gn * ldb + k0 + lc)
-                     : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto lstore = [&](int buf) {
+  for (int r = 0; r < G::A_ROUNDS; ++r) {
+    const int row = (r * G::NW + wave) * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz128(row);
+    asrc[r] = reinterpret_cast<const char*>(A + (int64_t)min(m0 + row, M - 1) * lda) + chunk * 16;
+  }
 #pragma unroll
-    for (int p = 0; p < G::PASSES; ++p) {
-      const int row = lr + p * G::RPP;
-      *reinterpret_cast<uint4*>(As + (buf * G::BM + row) * G::LDK + lc) = ra[p];
-      *reinterpret_cast<uint4*>(Bs + (buf * G::BN + row) * G::LDK + lc) = rb[p];
-    }
+  for (int r = 0; r < G::B_ROUNDS; ++r) {
+    const int row = (r * G::NW + wave) * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz128(row);
+    bsrc[r] = reinterpret_cast<const char*>(B + (int64_t)min(n0 + row, N - 1) * ldb) + chunk * 16;
+  }
+  auto issue = [&](int kt, int stage) {
+    char* base = smem + stage * G::STAGE_BYTES;
+#pragma unroll
+    for (int r = 0; r < G::A_ROUNDS; ++r) dma16(asrc[r] + kt * 128, base + (r * G::NW + wave) * 1024);
+#pragma unroll
+    for (int r = 0; r < G::B_ROUNDS; ++r)
+      dma16(bsrc[r] + kt * 128, base + G::BM * 128 + (r * G::NW + wave) * 1024);
   };
 
-  f32x4 acc[G::TM][G::TN];
+  f32x16 acc[G::TM][G::TN];
 #pragma unroll
   for (int i = 0; i < G::TM; ++i)
 #pragma unroll
-    for (int j = 0; j < G::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < G::TN; ++j) acc[i][j] = f32x16{};
 
   const int KT = K / G::BK;
-  const int fr = lane & 15, fk = (lane >> 4) * MM::KPL;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < G::STAGES - 1; ++st)
+    if (st < KT) issue(st, st);
+
+  // fragment rows: wm + i*32 + (lane & 31); all share swizzle ((lane & 15) >> 1)
+  const int fr = lane & 31, fsw = (lane & 15) >> 1;
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * G::BK);
-    const T* as = As + cur * G::BM * G::LDK;
-    const T* bs = Bs + cur * G::BN * G::LDK;
+    wait_slab<G::OPS, G::STAGES - 2>(min(G::STAGES - 2, KT - 1 - kt));
+    __builtin_amdgcn_s_barrier();
+    if (kt + G::STAGES - 1 < KT) issue(kt + G::STAGES - 1, (kt + G::STAGES - 1) % G::STAGES);
+
+    const char* as = smem + (kt % G::STAGES) * G::STAGE_BYTES;
+    const char* bs = as + G::BM * 128;
 #pragma unroll
     for (int ks = 0; ks < G::BK; ks += MM::KSTEP) {
+      const int k = ks + (lane >> 5) * MM::KPL;
+      const int cofs = (((k / G::VEC) ^ fsw) << 4) + (k % G::VEC) * (int)sizeof(T);
       frag af[G::TM], bfr[G::TN];
 #pragma unroll
       for (int i = 0; i < G::TM; ++i)
-        af[i] = load_frag<T, frag>(as + (wm + i * 16 + fr) * G::LDK + ks + fk);
+        af[i] = *reinterpret_cast<const frag*>(as + (wm + i * 32 + fr) * 128 + cofs);
 #pragma unroll
       for (int j = 0; j < G::TN; ++j)
-        bfr[j] = load_frag<T, frag>(bs + (wn + j * 16 + fr) * G::LDK + ks + fk);
+        bfr[j] = *reinterpret_cast<const frag*>(bs + (wn + j * 32 + fr) * 128 + cofs);
 #pragma unroll
       for (int i = 0; i < G::TM; ++i)
 #pragma unroll
         for (int j = 0; j < G::TN; ++j) acc[i][j] = MM::mma(af[i], bfr[j], acc[i][j]);
     }
-    if (kt + 1 < KT) lstore(cur ^ 1);
-    __syncthreads();
   }
 
+  // Epilogue in two column halves: the waves owning half p stage their
+  // accumulators (32x32 layout: lane holds column lane%32, register
+  // v holds row (v/4)*8 + (lane/32)*4 + v%4), then all threads run the
+  // epilogue on that half.
   float* Cs = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int i = 0; i < G::TM; ++i)
+  for (int p = 0; p < 2; ++p) {
+    __syncthreads();  // ring (or the previous half) no longer read
+    if ((wave & 1) == p) {
 #pragma unroll
-    for (int j = 0; j < G::TN; ++j)
+      for (int i = 0; i < G::TM; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        Cs[(wm + i * 16 + (lane >> 4) * 4 + e) * G::LDC + wn + j * 16 + fr] = acc[i][j][e];
-  __syncthreads();
-  epi(Cs, m0, n0, M, N);
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            Cs[(wm + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * G::LDC + j * 32 + fr] =
+                acc[i][j][v];
+    }
+    __syncthreads();
+    epi.template run<G::BM, G::HC, G::LDC>(Cs, m0, n0 + p * G::HC, M, N);
+  }
 }
 
+template <typename T, typename G, typename Epi>
+static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N,
+                               int K, const Epi& epi, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  dim3 grid((N + G::BN - 1) / G::BN, (M + G::BM - 1) / G::BM);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, G, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K,
+                     epi);
+  return hipGetLastError();
+}
+
+// 128x128 tiles.  Grids of more than one workgroup per CU use a two-slab
+// ring (64 KB, two workgroups resident per CU hide each other's latency);
+// grids that fit in one pass over the 256 CUs use a three-slab ring instead.
 template <typename T, typename Epi>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                          const Epi& epi, hipStream_t s) {
-  using G = GemmTile<T>;
-  if (M <= 0 || N <= 0) return hipSuccess;
-  dim3 grid((N + G::BN - 1) / G::BN, (M + G::BM - 1) / G::BM);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K, epi);
-  return hipGetLastError();
+  const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+  if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 2, 3>>(A, lda, B, ldb, M, N, K, epi, s);
+  return launch_tiled<T, GemmTile<T, 2, 2, 2>>(A, lda, B, ldb, M, N, K, epi, s);
 }
 
 template <typename T>
