@@ -12,6 +12,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.hip", "gemm.hip", "attention.hip", "rowops.hip"]
+# Per-source code generation options.  The attention kernel's score and
+# output accumulators are read by VALU code every key tile; keeping MFMA
+# operands in VGPRs avoids a copy out of the accumulation registers per tile.
+EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 LIB = os.path.join(HERE, "libcacherepair.so")
 ARCH = "gfx950"
 CFLAGS = [
@@ -40,7 +44,8 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        jobs.append(([_hipcc(), *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj], obj))
+        jobs.append(([_hipcc(), *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src),
+                      "-o", obj], obj))
     workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", "4"))))
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
         for out in ex.map(_run, [j[0] for j in jobs]):

@@ -28,9 +28,10 @@
 
 namespace cr {
 
-template <typename T, int D>
+template <typename T, int D, int STAGES_ = 3>
 struct AttnCfg {
-  static constexpr int BQ = 128, BKV = 64, STAGES = 4;
+  static constexpr int BQ = 128, BKV = 64, STAGES = STAGES_;
+  static constexpr int GROUPS = 2, NT = 256 * GROUPS;  // two 4-wave groups
   static constexpr int VEC = 16 / (int)sizeof(T);
   static constexpr int RBK = D * (int)sizeof(T);      // K tile row bytes
   static constexpr int RBV = BKV * (int)sizeof(T);    // V^T tile row bytes
@@ -38,6 +39,10 @@ struct AttnCfg {
   static constexpr int K_ROUNDS = K_BYTES / 4096, V_ROUNDS = V_BYTES / 4096;
   static constexpr int OPS = K_ROUNDS + V_ROUNDS;     // DMA ops per thread per tile
   static constexpr int STAGE_BYTES = K_BYTES + V_BYTES;
+  static constexpr int RING_BYTES = STAGES * STAGE_BYTES;
+  // merge area: group 1 hands (m, l, O^T) of its 128 queries to group 0
+  static constexpr int MERGE_BYTES = BQ * D * 4 + 2 * BQ * 2 * 4;
+  static constexpr int LDS = GROUPS * RING_BYTES > MERGE_BYTES ? GROUPS * RING_BYTES : MERGE_BYTES;
 };
 
 // A-operand row r of a 32-key sub-tile reads key swap_bits23(r).
@@ -47,8 +52,14 @@ __device__ __forceinline__ int swap_bits23(int r) {
 // Key (within a 32-key sub-tile) held by score register i of lane half g.
 __device__ __forceinline__ int score_key(int g, int i) { return (i >> 3) * 16 + g * 8 + (i & 7); }
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
+// Two groups of four waves share the 128 queries of a workgroup and split
+// its key tiles (group 0 even, group 1 odd tiles), each with its own online
+// softmax state and LDS ring; group 1's partial result is merged into group
+// 0's at the end.  This halves the critical path of the long query tiles of
+// late chunks and keeps two waves per SIMD so that one wave's softmax
+// overlaps the other's MFMAs.
+template <typename T, int D, int STAGES = 3>
+__global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
                                                         const T* __restrict__ Kg,
                                                         const T* __restrict__ Vt,
                                                         T* __restrict__ O, int N, int d_b,
@@ -56,7 +67,7 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
                                                         const int* __restrict__ lo_arr,
                                                         const int* __restrict__ hi_arr,
                                                         float scale_log2, int n_qtiles) {
-  using C = AttnCfg<T, D>;
+  using C = AttnCfg<T, D, STAGES>;
   using MM = Mma32<T>;
   using frag = typename MM::frag;
   using SK = Swz<C::RBK>;
@@ -64,23 +75,25 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
   constexpr int KPL = MM::KPL, KSTEP = MM::KSTEP;
   constexpr int QF = D / KSTEP;          // Q fragments per lane
   constexpr int DT = D / 32;             // 32-row tiles of O^T
-  __shared__ __align__(1024) char ring[C::STAGES * C::STAGE_BYTES];
+  __shared__ __align__(1024) char lds[C::LDS];
   __shared__ int red[2][4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2, gw = wave & 3, gtid = tid & 255;
   const int g = lane >> 5, ql = lane & 31;
   const int head = blockIdx.x % n_heads;
   const int qt = n_qtiles - 1 - blockIdx.x / n_heads;   // latest (longest) tiles first
-  const int q = qt * C::BQ + wave * 32 + ql;
+  const int q = qt * C::BQ + gw * 32 + ql;
   const bool qvalid = q < N;
   const int lo = qvalid ? lo_arr[q] : 0;
   const int hi = qvalid ? hi_arr[q] : 0;
+  char* ring = lds + grp * C::RING_BYTES;
 
-  // key range of the workgroup and mask-free window of this wave
+  // key range of the workgroup and mask-free window of this wave's queries
   {
     const int wlo = wave_min(qvalid ? lo : INT_MAX);
     const int whi = wave_max(qvalid ? hi : 0);
-    if (lane == 0) { red[0][wave] = wlo; red[1][wave] = whi; }
+    if (lane == 0 && grp == 0) { red[0][gw] = wlo; red[1][gw] = whi; }
   }
   const int wmax_lo = wave_max(qvalid ? lo : INT_MIN);
   const int wmin_hi = wave_min(qvalid ? hi : INT_MAX);
@@ -90,6 +103,8 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
   const int kv_end = max(max(red[1][0], red[1][1]), max(red[1][2], red[1][3]));
   const int kb = (kv_begin / C::BKV) * C::BKV;
   const int ntiles = (kv_end - kb + C::BKV - 1) / C::BKV;
+  const int iters = (ntiles + 1) / 2;                  // tiles per group (group 1 may idle last)
+  const int mine = (ntiles - grp + 1) / 2;             // tiles this group owns
 
   // Q^T fragments stay in registers: col = query, k = d
   frag qf[QF];
@@ -99,21 +114,21 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
     else qf[s] = frag{};
   }
 
-  // DMA sources (per lane, for the tile starting at key kb): K rows are keys
-  // (clamped to N-1 past the end: such keys are always masked), V^T rows are d.
+  // DMA sources (per lane): K rows are keys (clamped to N-1 past the end:
+  // such keys are always masked), V^T rows are d.
   const char* ksrc[C::K_ROUNDS];
   const char* vsrc[C::V_ROUNDS];
   int krow0[C::K_ROUNDS];
 #pragma unroll
   for (int r = 0; r < C::K_ROUNDS; ++r) {
-    const int row = (r * 4 + wave) * SK::RPW + lane / SK::CPR;
+    const int row = (r * 4 + gw) * SK::RPW + lane / SK::CPR;
     krow0[r] = row;
     const int chunk = SK::slot(row, lane % SK::CPR);
     ksrc[r] = reinterpret_cast<const char*>(Kg + head * D) + chunk * 16;
   }
 #pragma unroll
   for (int r = 0; r < C::V_ROUNDS; ++r) {
-    const int row = (r * 4 + wave) * SV::RPW + lane / SV::CPR;
+    const int row = (r * 4 + gw) * SV::RPW + lane / SV::CPR;
     const int chunk = SV::slot(row, lane % SV::CPR);
     vsrc[r] = reinterpret_cast<const char*>(Vt + ((int64_t)head * D + row) * n_pad + kb) + chunk * 16;
   }
@@ -125,34 +140,38 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
   float m_ref = -INFINITY, lsum = 0.f;
   const int krow = swap_bits23(ql);
 
-#define CR_ATTN_ISSUE(TILE, STAGE)                                                         \
+  // group-local tile i is workgroup tile 2i + grp
+#define CR_ATTN_ISSUE(I, STAGE)                                                            \
   do {                                                                                     \
     char* base_ = ring + (STAGE) * C::STAGE_BYTES;                                         \
-    const int k0_ = kb + (TILE) * C::BKV;                                                  \
+    const int tile_ = 2 * (I) + grp;                                                       \
+    const int k0_ = kb + tile_ * C::BKV;                                                   \
     _Pragma("unroll") for (int r = 0; r < C::K_ROUNDS; ++r) {                              \
       const int key_ = min(k0_ + krow0[r], N - 1);                                         \
-      dma16(ksrc[r] + key_ * krow_bytes, base_ + (r * 4 + wave) * 1024);                   \
+      dma16(ksrc[r] + key_ * krow_bytes, base_ + (r * 4 + gw) * 1024);                     \
     }                                                                                      \
     _Pragma("unroll") for (int r = 0; r < C::V_ROUNDS; ++r)                                \
-      dma16(vsrc[r] + (int64_t)(TILE) * C::BKV * sizeof(T),                                \
-            base_ + C::K_BYTES + (r * 4 + wave) * 1024);                                   \
+      dma16(vsrc[r] + (int64_t)tile_ * C::BKV * sizeof(T),                                 \
+            base_ + C::K_BYTES + (r * 4 + gw) * 1024);                                     \
   } while (0)
 
 #pragma unroll
   for (int st = 0; st < C::STAGES - 1; ++st)
-    if (st < ntiles) CR_ATTN_ISSUE(st, st);
+    if (st < mine) CR_ATTN_ISSUE(st, st);
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int ahead = min(C::STAGES - 2, ntiles - 1 - t);
-    if (ahead >= 2) wait_vmcnt<2 * C::OPS>();
-    else if (ahead == 1) wait_vmcnt<C::OPS>();
+  for (int it = 0; it < iters; ++it) {
+    // this group's slab `it` has landed once min(STAGES-2, mine-1-it) later ones remain
+    const int ahead = min(C::STAGES - 2, mine - 1 - it);
+    if (C::STAGES >= 4 && ahead >= 2) wait_vmcnt<2 * C::OPS>();
+    else if (C::STAGES >= 3 && ahead >= 1) wait_vmcnt<C::OPS>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    if (t + C::STAGES - 1 < ntiles) CR_ATTN_ISSUE(t + C::STAGES - 1, (t + C::STAGES - 1) % C::STAGES);
+    if (it + C::STAGES - 1 < mine) CR_ATTN_ISSUE(it + C::STAGES - 1, (it + C::STAGES - 1) % C::STAGES);
+    if (it >= mine) continue;   // group 1 without a last tile: only keeps the barrier count
 
-    const char* ks_ = ring + (t % C::STAGES) * C::STAGE_BYTES;
+    const char* ks_ = ring + (it % C::STAGES) * C::STAGE_BYTES;
     const char* vs_ = ks_ + C::K_BYTES;
-    const int k0 = kb + t * C::BKV;
+    const int k0 = kb + (2 * it + grp) * C::BKV;
 
     // S^T for two 32-key sub-tiles
     f32x16 s[2];
@@ -226,8 +245,29 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
   }
 #undef CR_ATTN_ISSUE
 
-  if (!qvalid) return;
-  const float total = lsum + __shfl_xor(lsum, 32, WAVE);
+  // merge group 1 into group 0: per query q' = gw*32 + ql, lane half g holds
+  // l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4 of O^T
+  __syncthreads();   // both rings idle
+  float* mo = reinterpret_cast<float*>(lds);                  // [BQ][D] O^T values
+  float* ml = mo + C::BQ * D;                                 // [BQ][2] (m, l) per lane half
+  const int qrow = gw * 32 + ql;
+  if (grp == 1) {
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        mo[qrow * D + d * 32 + (v >> 2) * 8 + g * 4 + (v & 3)] = oacc[d][v];
+    ml[(qrow * 2 + g) * 2 + 0] = m_ref;
+    ml[(qrow * 2 + g) * 2 + 1] = lsum;
+  }
+  __syncthreads();
+  if (grp == 1 || !qvalid) return;
+  const float m1 = ml[(qrow * 2 + g) * 2 + 0], l1 = ml[(qrow * 2 + g) * 2 + 1];
+  const float mt = fmaxf(m_ref, m1);
+  const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mt);
+  const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mt);
+  const float lpart = lsum * a0 + l1 * a1;
+  const float total = lpart + __shfl_xor(lpart, 32, WAVE);
   const float inv = 1.0f / total;
   T* orow = O + (int64_t)q * d_b + head * D;
 #pragma unroll
@@ -237,7 +277,8 @@ __global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ Q,
       const int dd = d * 32 + i4 * 8 + g * 4;
       T outv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) outv[e] = from_f32<T>(oacc[d][i4 * 4 + e] * inv);
+      for (int e = 0; e < 4; ++e)
+        outv[e] = from_f32<T>((oacc[d][i4 * 4 + e] * a0 + mo[qrow * D + dd + e] * a1) * inv);
       if constexpr (sizeof(T) == 2) {
         *reinterpret_cast<uint2*>(orow + dd) = *reinterpret_cast<const uint2*>(outv);
       } else {
@@ -253,11 +294,12 @@ hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, 
   const int n_qtiles = (N + 127) / 128;
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)d_head));
   dim3 grid(n_qtiles * n_heads);
+  constexpr int kStages = sizeof(T) == 2 ? 3 : 2;   // two rings must fit in 160 KB of LDS
   if (d_head == 64) {
-    hipLaunchKernelGGL((attention_kernel<T, 64>), grid, dim3(256), 0, s, q, k, vt, o, N, d_b,
+    hipLaunchKernelGGL((attention_kernel<T, 64, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
                        n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
   } else if (d_head == 32) {
-    hipLaunchKernelGGL((attention_kernel<T, 32>), grid, dim3(256), 0, s, q, k, vt, o, N, d_b,
+    hipLaunchKernelGGL((attention_kernel<T, 32, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
                        n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
   } else {
     return hipErrorInvalidValue;
