@@ -62,7 +62,7 @@ def algorithmic_work(w):
         "gemm_compress": (*gemm(dc, kc), 1),
         "gemm_token": (*gemm(db, E), 1),
         "gemm_fuse": (*gemm(db, dc + db), 1),
-        "gemm_inject": tuple(x * B for x in gemm(db, dc)) + (B,),
+        "gemm_inject": (*gemm(B * db, dc), 1),         # all blocks' P_b(s) in one launch
         "gemm_qkv": tuple(x * B for x in gemm(3 * db, db)) + (B,),
         "attention": (4.0 * allowed_pairs(w) * db * B, es * 4 * N * db * B, B),
         "gemm_oproj": tuple(x * B for x in gemm(db, db)) + (B,),

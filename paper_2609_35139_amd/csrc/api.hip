@@ -150,14 +150,16 @@ std::vector<Tensor> canonical(const cr_dims* d, const cr_kv_layout* l, uint64_t*
 }
 
 struct BlockP {
-  uint64_t w_inj, b_inj, ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_ff1, b_ff1, w_ff2,
-      b_ff2;
+  uint64_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_ff1, b_ff1, w_ff2, b_ff2;
 };
 // Prepared (device-optimised) weights: matrices [out][in] in the storage
-// dtype, vectors fp32.
+// dtype, vectors fp32.  The reinjection projections of all blocks are stacked
+// into one [B*d_b][d_c] matrix so that P_b(s) is computed for every block by
+// a single GEMM.
 struct Prepared {
   int64_t kc, kc_pad;
   uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_tok, b_tok, w_fuse, b_fuse;
+  uint64_t w_inj, b_inj;
   std::vector<BlockP> blk;
   uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta, total;
 };
@@ -176,9 +178,9 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
   p.b_cmp = a.take(dc * F); p.ln_enc_g = a.take(dc * F); p.ln_enc_b = a.take(dc * F);
   p.w_tok = a.take(db * E * T); p.b_tok = a.take(db * F);
   p.w_fuse = a.take(db * (dc + db) * T); p.b_fuse = a.take(db * F);
+  p.w_inj = a.take(d->n_blocks * db * dc * T); p.b_inj = a.take(d->n_blocks * db * F);
   for (int b = 0; b < d->n_blocks; ++b) {
     BlockP q;
-    q.w_inj = a.take(db * dc * T); q.b_inj = a.take(db * F);
     q.ln1_g = a.take(db * F); q.ln1_b = a.take(db * F);
     q.w_qkv = a.take(3 * db * db * T); q.b_qkv = a.take(3 * db * F);
     q.w_o = a.take(db * db * T); q.b_o = a.take(db * F);
@@ -194,8 +196,8 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
 }
 
 struct Workspace {
-  int64_t n, n_pad, ldst;
-  uint64_t lo, hi, pos, rope, U, st, h, a, q, k, vt, o, f, total;
+  int64_t n, n_pad, ldst, ldinj;
+  uint64_t lo, hi, pos, rope, U, st, inj, h, a, q, k, vt, o, f, total;
 };
 
 Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
@@ -207,11 +209,13 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.n = N;
   w.n_pad = round_up(std::max<int64_t>(N, 1), 128);
   w.ldst = dc + db;
+  w.ldinj = (int64_t)d->n_blocks * db;
   Arena a;
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
   w.rope = a.take(std::max<int64_t>(N, 1) * (dhd / 2) * 8);
   w.U = a.take(N * kc_pad * T);
   w.st = a.take(N * w.ldst * T);
+  w.inj = a.take(N * w.ldinj * T);
   w.h = a.take(N * db * T);
   w.a = a.take(N * db * T);
   w.q = a.take(N * db * T);
@@ -300,8 +304,8 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
   for (int b = 0; b < d->n_blocks; ++b) {
     const std::string q = "blk" + std::to_string(b) + ".";
     const BlockP& B = p.blk[b];
-    CR_TRY(mat(q + "w_inj", B.w_inj, dc, db, dc));
-    CR_TRY(vec(q + "b_inj", B.b_inj, db));
+    CR_TRY(mat(q + "w_inj", p.w_inj + (uint64_t)b * db * dc * sizeof(T), dc, db, dc));
+    CR_TRY(vec(q + "b_inj", p.b_inj + (uint64_t)b * db * 4, db));
     CR_TRY(vec(q + "ln1_g", B.ln1_g, db));
     CR_TRY(vec(q + "ln1_b", B.ln1_b, db));
     CR_TRY(mat(q + "w_qkv", B.w_qkv, db, 3 * db, db));
@@ -342,8 +346,10 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   int* hi = reinterpret_cast<int*>(ws + W.hi);
   int* pos = reinterpret_cast<int*>(ws + W.pos);
   float2* rope = reinterpret_cast<float2*>(ws + W.rope);
-  T *U = WT(W.U), *st = WT(W.st), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q), *k = WT(W.k),
-    *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
+  T *U = WT(W.U), *st = WT(W.st), *inj = WT(W.inj), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q),
+    *k = WT(W.k), *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
+  const int64_t ldinj = W.ldinj;
+  const int B = d->n_blocks;
   const cr::KvStrides ks{l->stride_layer, l->stride_kv, l->stride_token, l->stride_head,
                          l->n_kv_heads, l->head_dim};
   const float eps = d->ln_eps;
@@ -361,35 +367,39 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
                           PF(P.b_cmp), nullptr, 0, false, s); }));
   CR_TRY(timed("layernorm", s, [&] {
       return cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s); }));
-  // token projection -> st[:, d_c:], fusion -> h^0
+  // reinjection P_b(s) + b_b of every block at once -> inj[:, b*d_b : (b+1)*d_b]
+  if (B > 0)
+    CR_TRY(timed("gemm_inject", s, [&] {
+        return cr::gemm_bias<T>(st, ldst, PT(P.w_inj), dc, M, B * db, dc, inj, ldinj,
+                                PF(P.b_inj), nullptr, 0, false, s); }));
+  // token projection -> st[:, d_c:]; fusion -> h^0, plus block 0's reinjection
   CR_TRY(timed("gemm_token", s, [&] {
       return cr::gemm_bias<T>(emb, E, PT(P.w_tok), E, M, db, E, st + dc, ldst, PF(P.b_tok), nullptr,
                           0, false, s); }));
   CR_TRY(timed("gemm_fuse", s, [&] {
       return cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
-                          nullptr, 0, false, s); }));
-  for (int b = 0; b < d->n_blocks; ++b) {
-    const BlockP& B = P.blk[b];
-    CR_TRY(timed("gemm_inject", s, [&] {
-        return cr::gemm_bias<T>(st, ldst, PT(B.w_inj), dc, M, db, dc, h, db, PF(B.b_inj), h, db,
-                            false, s); }));
+                          B > 0 ? inj : nullptr, ldinj, false, s); }));
+  // h holds x_b = h^{b-1} + P_b(s) on entry to block b, h^B after the last block
+  for (int b = 0; b < B; ++b) {
+    const BlockP& Bk = P.blk[b];
+    const T* next_inj = b + 1 < B ? inj + (int64_t)(b + 1) * db : nullptr;
     CR_TRY(timed("layernorm", s, [&] {
-        return cr::layernorm<T>(h, db, a, db, PF(B.ln1_g), PF(B.ln1_b), M, db, eps, s); }));
+        return cr::layernorm<T>(h, db, a, db, PF(Bk.ln1_g), PF(Bk.ln1_b), M, db, eps, s); }));
     CR_TRY(timed("gemm_qkv", s, [&] {
-        return cr::gemm_qkv<T>(a, db, PT(B.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(B.b_qkv),
+        return cr::gemm_qkv<T>(a, db, PT(Bk.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(Bk.b_qkv),
                            pos, rope, s); }));
     CR_TRY(timed("attention", s, [&] {
         return cr::attention<T>(q, k, vt, o, M, db, nh, dhd, W.n_pad, lo, hi, s); }));
     CR_TRY(timed("gemm_oproj", s, [&] {
-        return cr::gemm_bias<T>(o, db, PT(B.w_o), db, M, db, db, h, db, PF(B.b_o), h, db, false, s); }));
+        return cr::gemm_bias<T>(o, db, PT(Bk.w_o), db, M, db, db, h, db, PF(Bk.b_o), h, db, false, s); }));
     CR_TRY(timed("layernorm", s, [&] {
-        return cr::layernorm<T>(h, db, a, db, PF(B.ln2_g), PF(B.ln2_b), M, db, eps, s); }));
+        return cr::layernorm<T>(h, db, a, db, PF(Bk.ln2_g), PF(Bk.ln2_b), M, db, eps, s); }));
     CR_TRY(timed("gemm_ffn1", s, [&] {
-        return cr::gemm_bias<T>(a, db, PT(B.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
-                            PF(B.b_ff1), nullptr, 0, true, s); }));
+        return cr::gemm_bias<T>(a, db, PT(Bk.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
+                            PF(Bk.b_ff1), nullptr, 0, true, s); }));
     CR_TRY(timed("gemm_ffn2", s, [&] {
-        return cr::gemm_bias<T>(f, (int64_t)r * db, PT(B.w_ff2), (int64_t)r * db, M, db, r * db, h,
-                            db, PF(B.b_ff2), h, db, false, s); }));
+        return cr::gemm_bias<T>(f, (int64_t)r * db, PT(Bk.w_ff2), (int64_t)r * db, M, db, r * db, h,
+                            db, PF(Bk.b_ff2), h, db, false, s, next_inj, ldinj); }));
   }
   CR_TRY(timed("layernorm", s, [&] {
       return cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s); }));

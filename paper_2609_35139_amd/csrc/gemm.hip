@@ -60,7 +60,8 @@ __device__ __forceinline__ void load8f(const float* p, float* v) {
 
 template <typename T>
 struct EpiBias {
-  T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; int gelu;
+  T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
+  int64_t ldr2; int gelu;
   template <int ROWS, int COLS, int LDC>
   __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS>;
@@ -68,12 +69,19 @@ struct EpiBias {
     if (gn >= N) return;
     float b[8];
     load8f(bias + gn, b);
-    Vec8<T> rv[S::PASSES];
+    Vec8<T> rv[S::PASSES], rv2[S::PASSES];
     if (resid) {
 #pragma unroll
       for (int p = 0; p < S::PASSES; ++p) {
         const int gm = m0 + S::row(p);
         if (gm < M) rv[p].load(resid + (int64_t)gm * ldr + gn);
+      }
+    }
+    if (resid2) {
+#pragma unroll
+      for (int p = 0; p < S::PASSES; ++p) {
+        const int gm = m0 + S::row(p);
+        if (gm < M) rv2[p].load(resid2 + (int64_t)gm * ldr2 + gn);
       }
     }
 #pragma unroll
@@ -91,6 +99,11 @@ struct EpiBias {
         float rf[8]; rv[p].to_float(rf);
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = rf[k] + v[k];
+      }
+      if (resid2) {
+        float rf[8]; rv2[p].to_float(rf);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = v[k] + rf[k];
       }
       Vec8<T> o; o.from_float(v); o.store(out + (int64_t)gm * ldo + gn);
     }
@@ -336,8 +349,8 @@ static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M
 template <typename T>
 hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                      T* out, int64_t ldo, const float* bias, const T* resid, int64_t ldr,
-                     bool gelu, hipStream_t s) {
-  EpiBias<T> e{out, ldo, bias, resid, ldr, gelu ? 1 : 0};
+                     bool gelu, hipStream_t s, const T* resid2, int64_t ldr2) {
+  EpiBias<T> e{out, ldo, bias, resid, ldr, resid2, ldr2, gelu ? 1 : 0};
   return launch<T>(A, lda, B, ldb, M, N, K, e, s);
 }
 
@@ -360,7 +373,8 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
 
 #define CR_INST(T)                                                                              \
   template hipError_t gemm_bias<T>(const T*, int64_t, const T*, int64_t, int, int, int, T*,    \
-                                   int64_t, const float*, const T*, int64_t, bool, hipStream_t); \
+                                   int64_t, const float*, const T*, int64_t, bool, hipStream_t, \
+                                   const T*, int64_t);                                          \
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*, \
                                   int64_t, const float*, const int*, const float2*, hipStream_t); \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides, \

@@ -14,11 +14,11 @@ struct KvStrides {
 };
 
 // ---- GEMM: C[M][N] = A[M][K] * B[N][K]^T, fp32 accumulation, K % 64 == 0.
-// Bias / GELU / residual epilogue: out = act(acc + bias) (+ resid).
+// Bias / GELU / residual epilogue: out = (resid +) act(acc + bias) (+ resid2).
 template <typename T>
 hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                      T* out, int64_t ldo, const float* bias, const T* resid, int64_t ldr,
-                     bool gelu, hipStream_t s);
+                     bool gelu, hipStream_t s, const T* resid2 = nullptr, int64_t ldr2 = 0);
 
 // QKV projection with the repair backbone's RoPE on Q and K (rotate-half
 // pairs, table rope[pos][d_head/2] of (cos, sin)); V is written transposed,

@@ -73,33 +73,39 @@ hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g,
 // u_g = (x_g / sigma_g) W1_g + b1_g for every segment g = (l, kv, h), with
 // 1/sigma folded into the prepared weights wseg[g][32][d_h] (rows >= d_seg
 // are zero).  One workgroup = 64 tokens of one segment, 16 tokens per wave,
-// 16x16 MFMA atoms fed straight from the cache rows (each lane reads one
-// 16-byte run of a token's head vector).
-template <typename T>
+// 16x16 MFMA atoms fed straight from the cache rows: every lane issues all
+// of its loads (one 16-byte run of its token's head vector per k-step, plus
+// the segment's weights) before the first product.
+template <typename T, int DH>
 __global__ __launch_bounds__(256) void compress_segments_kernel(
     const T* __restrict__ kv, KvStrides ks, const T* __restrict__ wseg,
     const float* __restrict__ bseg, T* __restrict__ U, int64_t ldu, int d_seg, int N, int Kc) {
   using MM = Mma16<T>;
   using frag = typename MM::frag;
+  constexpr int NK = DH / MM::KSTEP;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = blockIdx.y;
-  const int dh = ks.head_dim;
   const int h = g % ks.n_kv_heads, lk = g / ks.n_kv_heads;
   const T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
                   (int64_t)h * ks.head;
   const int t0 = blockIdx.x * 64 + wave * 16;
   const int tr = t0 + (lane & 15);
   const int fk = (lane >> 4) * MM::KPL;
-  const T* wg = wseg + (int64_t)g * 32 * dh;
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-  for (int k0 = 0; k0 < dh; k0 += MM::KSTEP) {
-    const frag a = tr < N ? load_frag<T, frag>(base + (int64_t)tr * ks.token + k0 + fk) : frag{};
+  const T* wg = wseg + (int64_t)g * 32 * DH;
+  frag a[NK], w[2][NK];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const frag bw = load_frag<T, frag>(wg + (j * 16 + (lane & 15)) * dh + k0 + fk);
-      acc[j] = MM::mma(a, bw, acc[j]);
-    }
-  }
+  for (int k = 0; k < NK; ++k)
+    a[k] = tr < N ? load_frag<T, frag>(base + (int64_t)tr * ks.token + k * MM::KSTEP + fk) : frag{};
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int k = 0; k < NK; ++k)
+      w[j][k] = load_frag<T, frag>(wg + (j * 16 + (lane & 15)) * DH + k * MM::KSTEP + fk);
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int k = 0; k < NK; ++k)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[j] = MM::mma(a[k], w[j][k], acc[j]);
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int col = j * 16 + (lane & 15);
@@ -128,8 +134,17 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
   if (N <= 0) return hipSuccess;
   const int S = 2 * n_layers * ks.n_kv_heads;
   dim3 grid((N + 63) / 64, S);
-  hipLaunchKernelGGL((compress_segments_kernel<T>), grid, dim3(256), 0, s, kv, ks, wseg, bseg, U,
-                     ldu, d_seg, N, S * d_seg);
+#define CR_COMPRESS(DH)                                                                        \
+  case DH:                                                                                     \
+    hipLaunchKernelGGL((compress_segments_kernel<T, DH>), grid, dim3(256), 0, s, kv, ks, wseg, \
+                       bseg, U, ldu, d_seg, N, S * d_seg);                                     \
+    break;
+  switch (ks.head_dim) {
+    CR_COMPRESS(32) CR_COMPRESS(64) CR_COMPRESS(96) CR_COMPRESS(128)
+    CR_COMPRESS(160) CR_COMPRESS(192) CR_COMPRESS(224) CR_COMPRESS(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef CR_COMPRESS
   return hipGetLastError();
 }
 
