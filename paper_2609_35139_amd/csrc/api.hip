@@ -10,9 +10,18 @@
 
 #include "launch.h"
 
+namespace cr {
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents le;
+  return le;
+}
+}  // namespace cr
+
 namespace {
 
 using cr::bf16;
+using cr::LaunchEvents;
+using cr::launch_events;
 
 constexpr uint64_t ALIGN = 256;
 inline uint64_t align_up(uint64_t x, uint64_t a = ALIGN) { return (x + a - 1) / a * a; }
@@ -252,9 +261,16 @@ hipError_t timed(const char* name, hipStream_t s, F&& f) {
       P.cls.emplace_back(name);
     }
   }
-  if (slot >= 0) hipEventRecord(P.ev[2 * slot], s);
+  if (slot < 0) return f();
+  LaunchEvents& le = launch_events();
+  le.start = P.ev[2 * slot];
+  le.stop = P.ev[2 * slot + 1];
   const hipError_t e = f();
-  if (slot >= 0) hipEventRecord(P.ev[2 * slot + 1], s);
+  if (le.start) {   // the stage launched nothing: an empty interval
+    hipEventRecord(P.ev[2 * slot], s);
+    hipEventRecord(P.ev[2 * slot + 1], s);
+  }
+  le = LaunchEvents{};
   return e;
 }
 

@@ -296,10 +296,10 @@ hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, 
   dim3 grid(n_qtiles * n_heads);
   constexpr int kStages = sizeof(T) == 2 ? 3 : 2;   // two rings must fit in 160 KB of LDS
   if (d_head == 64) {
-    hipLaunchKernelGGL((attention_kernel<T, 64, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
+    CR_LAUNCH((attention_kernel<T, 64, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
                        n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
   } else if (d_head == 32) {
-    hipLaunchKernelGGL((attention_kernel<T, 32, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
+    CR_LAUNCH((attention_kernel<T, 32, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
                        n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
   } else {
     return hipErrorInvalidValue;

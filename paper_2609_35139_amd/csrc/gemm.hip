@@ -330,7 +330,7 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
                                int K, const Epi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   dim3 grid((N + G::BN - 1) / G::BN, (M + G::BM - 1) / G::BM);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, G, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K,
+  CR_LAUNCH((gemm_nt_kernel<T, G, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K,
                      epi);
   return hipGetLastError();
 }

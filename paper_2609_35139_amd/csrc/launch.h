@@ -1,11 +1,30 @@
 // Host-side launchers of the CacheRepair kernels (internal to the library).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "common.h"
 
 namespace cr {
+
+// Profiler events of the stage being enqueued (both null when profiling is
+// off).  They are attached to the kernel dispatches themselves, so the pair
+// brackets the execution of the stage's kernels on the GPU, not the enqueue:
+// the first dispatch of the stage takes the start event, every dispatch the
+// stop event.  Thread-local, set around each stage by the library's profiler.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+#define CR_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                                 \
+  do {                                                                                  \
+    ::cr::LaunchEvents& le_ = ::cr::launch_events();                                     \
+    hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, le_.start, le_.stop, 0,    \
+                          __VA_ARGS__);                                                 \
+    le_.start = nullptr;                                                                \
+  } while (0)
 
 // Cache layout as seen by the kernels (elements).
 struct KvStrides {

@@ -11,6 +11,11 @@
 
 namespace cr {
 
+__device__ __forceinline__ void load8(const float* p, float* v) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
 // ------------------------------------------------------------- LayerNorm
 // y = (x - mean) / sqrt(var + eps) * g + b over rows of C elements, biased
 // variance, statistics in fp32 from values held in registers (two passes).
@@ -25,13 +30,22 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x,
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
   const T* xr = x + (int64_t)row * ldx;
-  float v[MAXV][8];
-  float sum = 0.f;
+  // every load (row, gamma, beta) is issued before the first reduction
+  float v[MAXV][8], gv[MAXV][8], bv[MAXV][8];
 #pragma unroll
   for (int k = 0; k < MAXV; ++k) {
     const int c = (k * 64 + lane) * 8;
     if (c < C) {
       Vec8<T> t; t.load(xr + c); t.to_float(v[k]);
+      load8(g + c, gv[k]);
+      load8(b + c, bv[k]);
+    }
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < C) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) sum += v[k][e];
     }
@@ -54,7 +68,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x,
     if (c < C) {
       float o[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (v[k][e] - mean) * rstd * g[c + e] + b[c + e];
+      for (int e = 0; e < 8; ++e) o[e] = (v[k][e] - mean) * rstd * gv[k][e] + bv[k][e];
       Vec8<T> t; t.from_float(o); t.store(yr + c);
     }
   }
@@ -64,7 +78,7 @@ template <typename T>
 hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g, const float* b,
                      int M, int C, float eps, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL((layernorm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
+  CR_LAUNCH((layernorm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
                      g, b, M, C, eps);
   return hipGetLastError();
 }
@@ -136,7 +150,7 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
   dim3 grid((N + 63) / 64, S);
 #define CR_COMPRESS(DH)                                                                        \
   case DH:                                                                                     \
-    hipLaunchKernelGGL((compress_segments_kernel<T, DH>), grid, dim3(256), 0, s, kv, ks, wseg, \
+    CR_LAUNCH((compress_segments_kernel<T, DH>), grid, dim3(256), 0, s, kv, ks, wseg, \
                        bseg, U, ldu, d_seg, N, S * d_seg);                                     \
     break;
   switch (ks.head_dim) {
@@ -188,7 +202,7 @@ hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* r
     for (int i = 0; i < sb.count; ++i) sb.req_start[i] = rs[c0 + i];
     const int ntok = sb.offs[sb.count] - sb.offs[0];
     if (ntok == 0) continue;
-    hipLaunchKernelGGL(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos);
+    CR_LAUNCH(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -209,7 +223,7 @@ hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStr
   const int half = d_head / 2;
   const int n = max_pos * half;
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos,
+  CR_LAUNCH(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos,
                      half, d_head, theta);
   return hipGetLastError();
 }
@@ -239,7 +253,7 @@ hipError_t transpose_convert(const Tin* src, Tout* dst, int batch, int R, int C,
   const int64_t n = (int64_t)Cp * ld_dst;
   if (n <= 0 || batch <= 0) return hipSuccess;
   dim3 grid((unsigned)((n + 255) / 256), 1, batch);
-  hipLaunchKernelGGL((transpose_convert_kernel<Tin, Tout>), grid, dim3(256), 0, s, src, dst, R, C,
+  CR_LAUNCH((transpose_convert_kernel<Tin, Tout>), grid, dim3(256), 0, s, src, dst, R, C,
                      Cp, ld_dst, div);
   return hipGetLastError();
 }
@@ -259,7 +273,7 @@ hipError_t convert_f32(const Tin* src, float* dst, int64_t n, int64_t n_pad, int
                        int64_t sb, int64_t db, hipStream_t s) {
   if (n_pad <= 0 || batch <= 0) return hipSuccess;
   dim3 grid((unsigned)((n_pad + 255) / 256), 1, batch);
-  hipLaunchKernelGGL((convert_f32_kernel<Tin>), grid, dim3(256), 0, s, src, dst, n, n_pad, sb, db);
+  CR_LAUNCH((convert_f32_kernel<Tin>), grid, dim3(256), 0, s, src, dst, n, n_pad, sb, db);
   return hipGetLastError();
 }
 

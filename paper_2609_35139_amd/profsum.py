@@ -1,0 +1,181 @@
+"""Text summaries of rocprofv3 output for the repair kernels.
+
+Two kinds of summary are written (short text files, a few KB):
+
+* ``kernel_stats``: the ``--kernel-trace --stats`` table of one command, with
+  the bench line of the same run appended;
+* ``traffic``: HBM bytes per launch of one kernel class from two ``--pmc``
+  passes (``FETCH_SIZE``, then ``WRITE_SIZE``; KiB per dispatch), each divided
+  by the factor the same counter reads for a device-to-device copy of known
+  size in the same process.  The file records a hash of the sources that
+  build the kernel, so a reader can tell whether the counters still describe
+  the current code.
+
+Usage::
+
+    python -m paper_2609_35139_amd.profsum stats <kernel_stats.csv> <bench.json> <out.txt> <command...>
+    python -m paper_2609_35139_amd.profsum traffic <fetch_counter_collection.csv> \
+        <write_counter_collection.csv> <bench.json> <class> <out.txt> <command...>
+"""
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+
+# kernel class -> (substring of the device function name, sources that build it)
+CLASS_KERNEL = {
+    "attention": ("attention_kernel", ["attention.hip", "common.h", "launch.h"]),
+    "layernorm": ("layernorm_kernel", ["rowops.hip", "common.h", "launch.h"]),
+    "compress_segments": ("compress_segments_kernel", ["rowops.hip", "common.h", "launch.h"]),
+    "gemm_expand": ("EpiExpand", ["gemm.hip", "common.h", "launch.h"]),
+    "gemm_qkv": ("EpiQKV", ["gemm.hip", "common.h", "launch.h"]),
+}
+for _c in ("gemm_compress", "gemm_token", "gemm_fuse", "gemm_inject", "gemm_oproj", "gemm_ffn1",
+           "gemm_ffn2"):
+    CLASS_KERNEL[_c] = ("EpiBias", ["gemm.hip", "common.h", "launch.h"])
+
+
+def source_hash(cls):
+    h = hashlib.sha256()
+    for f in CLASS_KERNEL[cls][1]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def bench_line(path):
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith('{"metric"'):
+                return json.loads(line)
+    raise ValueError(f"no bench JSON line in {path}")
+
+
+def short_name(n):
+    n = re.sub(r"\(.*", "", n)
+    for k in ("EpiBias", "EpiQKV", "EpiExpand"):
+        if k in n:
+            return "gemm_nt_kernel<" + k + ">"
+    m = re.search(r"cr::(\w+)|_ZN2cr\d+(\w+?)I|_ZN2cr\d+(\w+)E", n)
+    return (m.group(1) or m.group(2) or m.group(3)) if m else n[:40]
+
+
+def kernel_stats(stats_csv, bench_json, command):
+    rows = list(csv.DictReader(open(stats_csv)))
+    b = bench_line(bench_json)
+    out = [f"# rocprofv3 kernel statistics: repair forward pass, workload {b['config']['workload']}",
+           f"# command: {command}",
+           "# (the bench runs warmup + timed + profiled passes; averages are per launch)",
+           "%-36s %8s %12s %10s %7s" % ("kernel", "calls", "total_us", "avg_us", "pct")]
+    for r in rows:
+        out.append("%-36s %8s %12.1f %10.2f %7.2f" % (
+            short_name(r["Name"]), r["Calls"], float(r["TotalDurationNs"]) / 1e3,
+            float(r["AverageNs"]) / 1e3, float(r["Percentage"])))
+    rf = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in b["roofline"].items()}
+    out += ["", "# bench line of the same command (live HIP events on the library's stream):",
+            "#   ms_per_step %.3f, value %.4g tokens/s" % (b["ms_per_step"], b["value"]),
+            "#   roofline " + json.dumps(rf),
+            "#   per-class average launch (us): " +
+            ", ".join("%s %.1f" % (k["class"], k["avg_us"]) for k in b["kernels"])]
+    return "\n".join(out) + "\n"
+
+
+def _per_dispatch(path, counter):
+    """{kernel name: [value per dispatch]} for one counter of a --pmc pass."""
+    vals = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        vals.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+        vals[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    return {k: list(v.values()) for k, v in vals.items()}
+
+
+def _calibration(per_kernel, copy_bytes):
+    """Counter bytes / true bytes of the device-to-device copy of copy_bytes."""
+    best = None
+    for name, vs in per_kernel.items():
+        if "copy" not in name.lower():
+            continue
+        for v in vs:
+            ratio = v * 1024.0 / copy_bytes
+            if 0.25 < ratio < 4.0 and (best is None or abs(ratio - 1) < abs(best - 1)):
+                best = ratio
+    if best is None:
+        raise ValueError("calibration copy not found among the profiled kernels")
+    return best
+
+
+def traffic(fetch_csv, write_csv, bench_json, cls, command):
+    b = bench_line(bench_json)
+    calib = b["calibration"]["copy_bytes"]
+    sub = CLASS_KERNEL[cls][0]
+    res = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        per = _per_dispatch(path, counter)
+        factor = _calibration(per, calib)
+        ks = [v for n, vs in per.items() if sub in n for v in vs]
+        if not ks:
+            raise ValueError(f"no dispatch of {sub} in {path}")
+        kib = sum(ks) / len(ks)
+        res[counter] = {"kib_per_dispatch": kib, "dispatches": len(ks), "copy_factor": factor,
+                        "bytes_per_launch": kib * 1024.0 / factor}
+    total = res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"]
+    algo = None
+    for k in b["kernels"]:
+        if k["class"] == cls and "gbs" in k:
+            algo = k["gbs"] * 1e9 * k["avg_us"] * 1e-6
+    out = [f"# HBM traffic per launch: {cls} ({sub}), workload {b['config']['workload']}",
+           f"# command (one pass per counter): {command}",
+           f"# calibration: device-to-device copy of {calib} bytes in the same process",
+           f"class: {cls}",
+           f"source_sha256: {source_hash(cls)}"]
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        r = res[counter]
+        out.append(f"{counter.lower()}_kib_per_dispatch: {r['kib_per_dispatch']:.1f}"
+                   f"  (mean of {r['dispatches']} dispatches; copy factor {r['copy_factor']:.4f})")
+    out.append(f"fetch_bytes_per_launch: {res['FETCH_SIZE']['bytes_per_launch']:.0f}")
+    out.append(f"write_bytes_per_launch: {res['WRITE_SIZE']['bytes_per_launch']:.0f}")
+    out.append(f"traffic_bytes_per_launch: {total:.0f}")
+    if algo:
+        out.append(f"algorithmic_bytes_per_launch: {algo:.0f}  (ratio {total / algo:.3f})")
+    return "\n".join(out) + "\n"
+
+
+def read_traffic(path, cls):
+    """Traffic bytes per launch recorded for cls, or None when the file is
+    missing or the kernel sources changed since the counters were taken."""
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.split()[0] if v.split() else ""
+    if kv.get("class") != cls or kv.get("source_sha256") != source_hash(cls):
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+def main(argv):
+    mode = argv[0]
+    if mode == "stats":
+        stats_csv, bench_json, out = argv[1:4]
+        text = kernel_stats(stats_csv, bench_json, " ".join(argv[4:]))
+    elif mode == "traffic":
+        fetch_csv, write_csv, bench_json, cls, out = argv[1:6]
+        text = traffic(fetch_csv, write_csv, bench_json, cls, " ".join(argv[6:]))
+    else:
+        raise SystemExit(__doc__)
+    with open(out, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])
