@@ -10,7 +10,14 @@ It is a plain, slow, step-by-step forward pass in float64, written from the
 paper's Section 4.1 ("Inference"): StaleEncoder and token fusion, Repair
 Blocks with stale-feature reinjection under the block-causal mask A_ij,
 final LayerNorm, KV Residual Head and the output skip add
-KV_hat = KV_stale + sigma_delta * z.  The readings taken where the paper is
+KV_hat = KV_stale + sigma_delta * z, optionally followed by placing K at its
+global request position, K_hat = R_M(p_t) K_hat^c (same section, "KV residual
+output and global RoPE").  The controlled variants of the appendix "Attention
+Topology and Within-Chunk Context" are options: token-causal (A1),
+bidirectional (A2) and block-diagonal (A3) masks, entrance-only stale
+features (A4: no per-block P_b), direct prediction with zero output offset
+(A5: KV_hat = sigma * z), and the output choices of Table
+tab:repair-components (repair K only, V only, keep the first chunk).  The readings taken where the paper is
 silent (LayerNorm on s, pre-LN blocks, exact-erf GELU, rotate-half RoPE with
 base 1e4 at 0-based positions within the request, biases on every linear,
 d_c != d_b handling) are listed in the design notes; each is a one-line
@@ -23,6 +30,13 @@ Pins (tests/test_oracle.py, CPU):
   masked_attention  pure-Python brute force over an explicit A_ij; one chunk ==
                     unmasked SDPA; length-1 chunks == causal SDPA; constant V
   block_causal_attention  equals masked_attention under the explicit A_ij
+  chunk_attention   every mask variant equals masked_attention under its
+                    explicit mask (brute-force definitions in the tests)
+  rotate_keys       complex-number form of the rotation; R(p)^-1 R(p) = I;
+                    R(0) = scale * I; V coordinates untouched
+  repair variants   A4 == method with w_inj = b_inj = 0; A5 == method - stale;
+                    K-only / V-only / keep-first-chunk select exact method
+                    values; global placement == rotate_keys(method output)
   stale_encoder     input-scale invariance (X*a, sigma*a); zero-weight closed
                     forms
   repair            zero head returns the stale cache exactly; bias-only head
@@ -43,10 +57,13 @@ from scipy.special import erf
 
 __all__ = [
     "layer_norm", "gelu", "rope", "token_chunk_ids", "token_request_ids",
-    "positions", "block_causal_allowed", "masked_attention", "block_causal_attention",
-    "stale_encoder",
-    "token_fusion", "repair_block", "repair_features", "apply_head", "repair",
+    "positions", "block_causal_allowed", "attention_allowed", "masked_attention",
+    "block_causal_attention", "chunk_attention", "stale_encoder",
+    "token_fusion", "repair_block", "repair_features", "apply_head", "key_columns",
+    "rotate_keys", "repair", "MASKS",
 ]
+
+MASKS = ("block_causal", "token_causal", "bidirectional", "block_diagonal")
 
 F64 = np.float64
 
@@ -126,6 +143,28 @@ def block_causal_allowed(chunk_ids: np.ndarray, request_ids: np.ndarray) -> np.n
     return (c[None, :] <= c[:, None]) & (r[None, :] == r[:, None])
 
 
+def attention_allowed(mask: str, chunk_ids: np.ndarray, request_ids: np.ndarray) -> np.ndarray:
+    """Explicit allowed-pair matrix of an attention topology (row = query i,
+    column = key j), always restricted to the query's request.
+
+    block_causal (A0, the method): c(j) <= c(i); token_causal (A1): j <= i;
+    bidirectional (A2): any key; block_diagonal (A3): c(j) == c(i).
+    """
+    c = np.asarray(chunk_ids)
+    r = np.asarray(request_ids)
+    same = r[None, :] == r[:, None]
+    if mask == "block_causal":
+        return same & (c[None, :] <= c[:, None])
+    if mask == "token_causal":
+        n = len(c)
+        return same & (np.arange(n)[None, :] <= np.arange(n)[:, None])
+    if mask == "bidirectional":
+        return same
+    if mask == "block_diagonal":
+        return same & (c[None, :] == c[:, None])
+    raise ValueError(f"unknown mask {mask!r}")
+
+
 def masked_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
                      allowed: np.ndarray) -> np.ndarray:
     """Softmax attention per head over the allowed keys.
@@ -155,17 +194,37 @@ def block_causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     first token of c's request up to the last token of c, so each chunk's
     rows attend, unmasked, to that contiguous key range.
     """
+    return chunk_attention(q, k, v, chunk_offsets, request_chunks, "block_causal")
+
+
+def chunk_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, chunk_offsets: np.ndarray,
+                    request_chunks: np.ndarray, mask: str) -> np.ndarray:
+    """Attention under one of the topologies of attention_allowed, computed
+    chunk by chunk: the rows of chunk c (tokens [a, b) of request [s, e))
+    see the contiguous keys [s, b) (block-causal), [s, e) (bidirectional) or
+    [a, b) (block-diagonal); token-causal uses the keys [s, b) with the
+    additional condition j <= i inside them."""
+    if mask not in MASKS:
+        raise ValueError(f"unknown mask {mask!r}")
     off = np.asarray(chunk_offsets, np.int64)
     rc = np.asarray(request_chunks, np.int64)
     out = np.empty(np.shape(q), F64)
     for r in range(len(rc) - 1):
-        start = off[rc[r]]
+        start, end = off[rc[r]], off[rc[r + 1]]
         for c in range(rc[r], rc[r + 1]):
             a, b = off[c], off[c + 1]
             if a == b:
                 continue
-            everything = np.ones((b - a, b - start), bool)
-            out[a:b] = masked_attention(q[a:b], k[start:b], v[start:b], everything)
+            if mask == "bidirectional":
+                k0, k1 = start, end
+            elif mask == "block_diagonal":
+                k0, k1 = a, b
+            else:
+                k0, k1 = start, b
+            allowed = np.ones((b - a, k1 - k0), bool)
+            if mask == "token_causal":
+                allowed = np.arange(k0, k1)[None, :] <= np.arange(a, b)[:, None]
+            out[a:b] = masked_attention(q[a:b], k[k0:k1], v[k0:k1], allowed)
     return out
 
 
@@ -199,13 +258,15 @@ def token_fusion(s: np.ndarray, token_embeds: np.ndarray, w: Dict[str, np.ndarra
 
 def repair_block(h: np.ndarray, s: np.ndarray, w: Dict[str, np.ndarray], b: int,
                  n_heads: int, chunk_offsets: np.ndarray, request_chunks: np.ndarray,
-                 pos: np.ndarray, rope_theta: float, ln_eps: float) -> np.ndarray:
-    """h^b = RepairBlock_b(h^{b-1} + P_b(s); A, p), a pre-LN Transformer block."""
+                 pos: np.ndarray, rope_theta: float, ln_eps: float,
+                 mask: str = "block_causal", reinject: bool = True) -> np.ndarray:
+    """h^b = RepairBlock_b(h^{b-1} + P_b(s); A, p), a pre-LN Transformer block.
+    reinject=False is variant A4 (stale features only at the entrance)."""
     p = f"blk{b}."
     W = lambda n: np.asarray(w[p + n], F64)
     N, db = h.shape
     d = db // n_heads
-    x = h + s @ W("w_inj") + W("b_inj")
+    x = h + s @ W("w_inj") + W("b_inj") if reinject else np.array(h, F64)
     a = layer_norm(x, W("ln1_g"), W("ln1_b"), ln_eps)
     qkv = a @ W("w_qkv") + W("b_qkv")
     q = qkv[:, 0 * db:1 * db].reshape(N, n_heads, d)
@@ -213,7 +274,7 @@ def repair_block(h: np.ndarray, s: np.ndarray, w: Dict[str, np.ndarray], b: int,
     v = qkv[:, 2 * db:3 * db].reshape(N, n_heads, d)
     q = rope(q, pos, rope_theta)
     k = rope(k, pos, rope_theta)
-    o = block_causal_attention(q, k, v, chunk_offsets, request_chunks).reshape(N, db)
+    o = chunk_attention(q, k, v, chunk_offsets, request_chunks, mask).reshape(N, db)
     x = x + o @ W("w_o") + W("b_o")
     f = gelu(layer_norm(x, W("ln2_g"), W("ln2_b"), ln_eps) @ W("w_ff1") + W("b_ff1"))
     return x + f @ W("w_ff2") + W("b_ff2")
@@ -223,7 +284,8 @@ def repair_features(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.n
                     request_chunks: Optional[np.ndarray], w: Dict[str, np.ndarray],
                     head_dim: int, n_heads: int, rope_theta: float = 1e4,
                     ln_eps: float = 1e-5, pos_shift: float = 0.0,
-                    taps: Optional[dict] = None) -> np.ndarray:
+                    taps: Optional[dict] = None, mask: str = "block_causal",
+                    reinject: bool = True) -> np.ndarray:
     """Everything up to LN_f(h^B): returns [N, d_b] in fp64."""
     if request_chunks is None:
         request_chunks = np.array([0, len(chunk_offsets) - 1], np.int32)
@@ -236,7 +298,7 @@ def repair_features(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.n
     n_blocks = sum(1 for k in w if k.endswith(".w_inj"))
     for b in range(n_blocks):
         h = repair_block(h, s, w, b, n_heads, chunk_offsets, request_chunks, pos,
-                         rope_theta, ln_eps)
+                         rope_theta, ln_eps, mask, reinject)
         if taps is not None:
             taps[f"h{b + 1}"] = h
     lnf = layer_norm(h, w["ln_f_g"], w["ln_f_b"], ln_eps)
@@ -246,22 +308,100 @@ def repair_features(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.n
 
 
 def apply_head(X_cols: np.ndarray, lnf: np.ndarray, w: Dict[str, np.ndarray],
-               cols: slice = slice(None)) -> np.ndarray:
+               cols: slice = slice(None), residual: bool = True) -> np.ndarray:
     """KV_hat = KV_stale + sigma_delta * (LN_f(h^B) @ W_out + b_out) on a
     column range of the cache (Section 4.1, KV residual output).  X_cols
-    holds the stale values of exactly those columns."""
+    holds the stale values of exactly those columns.  residual=False is
+    variant A5: direct prediction with zero output offset, sigma * z."""
     z = lnf @ np.asarray(w["w_out"][:, cols], F64)
     z += np.asarray(w["b_out"][cols], F64)            # z = LN_f(h) W_out + b_out
     z *= np.asarray(w["sigma_delta"][cols], F64)      # sigma_delta * z
-    z += np.asarray(X_cols, F64)                      # stale + sigma_delta * z
+    if residual:
+        z += np.asarray(X_cols, F64)                  # stale + sigma_delta * z
     return z
+
+
+def key_columns(n_layers: int, n_kv_heads: int, head_dim: int) -> np.ndarray:
+    """Boolean [D_KV]: coordinate j = ((l*2 + kv)*H + h)*d_h + i is a K entry."""
+    seg = np.arange(2 * n_layers * n_kv_heads * head_dim) // head_dim
+    return (seg // n_kv_heads) % 2 == 0
+
+
+def rotate_keys(Y: np.ndarray, positions: np.ndarray, inv_freq: np.ndarray,
+                n_layers: int, n_kv_heads: int, head_dim: int, scale: float = 1.0,
+                inverse: bool = False) -> np.ndarray:
+    """Target-model rotary encoding R_M(p_t) applied to every K head of a
+    canonical-coordinate cache Y [N, D_KV] (Section 4.1, "Chunk-cache
+    preparation" and "KV residual output and global RoPE").  Rotate-half
+    pairs (i, i + d_h/2) turn by p_t * inv_freq[i]; both outputs are
+    multiplied by scale (1 for plain RoPE).  inverse=True applies
+    R_M(p_t)^-1.  V coordinates are returned unchanged."""
+    Y = np.array(Y, F64)
+    half = head_dim // 2
+    ang = np.asarray(positions, F64)[:, None] * np.asarray(inv_freq, F64)[None, :half]
+    if inverse:
+        ang = -ang
+    cos, sin = np.cos(ang), np.sin(ang)
+    s = (1.0 / scale) if inverse else scale
+    S = 2 * n_layers * n_kv_heads
+    for g in range(S):
+        if (g // n_kv_heads) % 2:
+            continue                                  # V segment: native coordinates
+        a = g * head_dim
+        x1 = Y[:, a:a + half].copy()
+        x2 = Y[:, a + half:a + head_dim].copy()
+        Y[:, a:a + half] = s * (x1 * cos - x2 * sin)
+        Y[:, a + half:a + head_dim] = s * (x2 * cos + x1 * sin)
+    return Y
 
 
 def repair(X: np.ndarray, token_embeds: np.ndarray, chunk_offsets: np.ndarray,
            request_chunks: Optional[np.ndarray], w: Dict[str, np.ndarray],
            head_dim: int, n_heads: int, rope_theta: float = 1e4, ln_eps: float = 1e-5,
-           pos_shift: float = 0.0, taps: Optional[dict] = None) -> np.ndarray:
-    """Repaired canonical cache [N, D_KV] in fp64 for stale cache X [N, D_KV]."""
+           pos_shift: float = 0.0, taps: Optional[dict] = None, *,
+           mask: str = "block_causal", reinject: bool = True, residual: bool = True,
+           apply: str = "kv", keep_first_chunk: bool = False,
+           n_kv_heads: Optional[int] = None, global_rope: Optional[dict] = None) -> np.ndarray:
+    """Repaired cache [N, D_KV] in fp64 for stale canonical cache X [N, D_KV].
+
+    Defaults give the method (block-causal, reinjection, residual output,
+    both components, canonical K).  apply in {"kv", "k", "v"} selects the
+    components that receive the network's output; keep_first_chunk leaves
+    the first chunk of every request at its stale values (Table
+    tab:repair-components; the network still runs on every token).
+    global_rope = {"inv_freq": [d_h/2], "scale": s, "position_offset":
+    [n_requests] or None} places every K at p_t = position_offset[req(t)] +
+    (position of t in its request) after the output add.  n_kv_heads is
+    needed to tell K from V coordinates (apply != "kv" or global_rope).
+    """
+    if request_chunks is None:
+        request_chunks = np.array([0, len(chunk_offsets) - 1], np.int32)
     lnf = repair_features(X, token_embeds, chunk_offsets, request_chunks, w, head_dim,
-                          n_heads, rope_theta, ln_eps, pos_shift, taps)
-    return apply_head(X, lnf, w)
+                          n_heads, rope_theta, ln_eps, pos_shift, taps, mask, reinject)
+    if apply == "kv" and not keep_first_chunk and global_rope is None:
+        return apply_head(X, lnf, w, residual=residual)
+    if n_kv_heads is None:
+        raise ValueError("n_kv_heads is required for output selection or global RoPE")
+    D = X.shape[1]
+    n_layers = D // (2 * n_kv_heads * head_dim)
+    is_k = key_columns(n_layers, n_kv_heads, head_dim)
+    cols = {"kv": np.ones(D, bool), "k": is_k, "v": ~is_k}[apply]
+    rows = np.ones(X.shape[0], bool)
+    off = np.asarray(chunk_offsets, np.int64)
+    rc = np.asarray(request_chunks, np.int64)
+    if keep_first_chunk:
+        for q in range(len(rc) - 1):
+            if rc[q] < rc[q + 1]:
+                rows[off[rc[q]]:off[rc[q] + 1]] = False
+    Y = np.array(X, F64)
+    ci = np.nonzero(cols)[0]
+    Y[np.ix_(rows, ci)] = apply_head(np.asarray(X, F64)[np.ix_(rows, ci)], lnf[rows], w, ci,
+                                     residual)
+    if global_rope is not None:
+        pos = positions(chunk_offsets, request_chunks)
+        po = global_rope.get("position_offset")
+        if po is not None:
+            pos = pos + np.asarray(po, np.int64)[token_request_ids(chunk_offsets, request_chunks)]
+        Y = rotate_keys(Y, pos, global_rope["inv_freq"], n_layers, n_kv_heads, head_dim,
+                        global_rope.get("scale", 1.0))
+    return Y

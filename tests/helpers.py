@@ -15,16 +15,20 @@ def small_workload(chunk_lengths, seed=11, dtype="f32", L=2, H=1, dh=8, E=16,
     return W.Workload("test", dtype, t, r, tuple(tuple(c) for c in chunk_lengths), seed)
 
 
-def oracle_repair(inp, taps=None, weights=None, pos_shift=0.0, X=None, embeds=None):
-    """Run the fp64 oracle on a workloads.Inputs bundle; returns [N, D_KV]."""
+def oracle_repair(inp, taps=None, weights=None, pos_shift=0.0, X=None, embeds=None, **options):
+    """Run the fp64 oracle on a workloads.Inputs bundle; returns [N, D_KV].
+    options: the variant keywords of oracle.repair (mask, reinject, residual,
+    apply, keep_first_chunk, global_rope)."""
     from oracle import repair
     w = inp.workload
     X = W.kv_layer_major_to_canonical(inp.kv) if X is None else X
+    if options:
+        options.setdefault("n_kv_heads", w.target.n_kv_heads)
     return repair(X, inp.token_embeds if embeds is None else embeds,
                   w.chunk_offsets, w.request_chunks,
                   inp.weights if weights is None else weights,
                   w.target.head_dim, w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps,
-                  pos_shift=pos_shift, taps=taps)
+                  pos_shift=pos_shift, taps=taps, **options)
 
 
 # ------------------------------------------------------------------ GPU side
