@@ -264,6 +264,35 @@ def main():
     if roofline["peak_measured"]:
         roofline["frac_of_measured"] = achieved / roofline["peak_measured"]
 
+    # variants behind cr_repair_ex on the same batch (the cache is repaired in
+    # place each step, as in the timed loop above)
+    variant_opts = {
+        "global_key_placement": B.Options(global_rope=dict(theta=1e6)),
+        "token_causal": B.Options(mask="token_causal"),
+        "bidirectional": B.Options(mask="bidirectional"),
+        "block_diagonal": B.Options(mask="block_diagonal"),
+        "entrance_only": B.Options(reinject=False),
+        "direct_prediction": B.Options(residual=False),
+        "repair_k_only": B.Options(apply="k"),
+        "repair_v_only": B.Options(apply="v"),
+        "keep_first_chunk": B.Options(keep_first_chunk=True),
+    }
+    variants = {}
+    vsteps = max(1, min(args.steps, 10))
+    for name, opt in variant_opts.items():
+        for _ in range(2):
+            rep.repair(kv, off, req, emb, workspace=ws, stream=stream, options=opt)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(vsteps):
+            rep.repair(kv, off, req, emb, workspace=ws, stream=stream, options=opt)
+        b.record(stream)
+        torch.cuda.synchronize()
+        vms = a.elapsed_time(b) / vsteps
+        variants[name] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
+    print("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in
+                                            variants.items()), file=sys.stderr, flush=True)
+
     cold = None
     if args.cold:
         flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -302,6 +331,7 @@ def main():
         "cpu_baseline": cpu,
         "cold_ms_per_step": cold,
         "measured_peaks": measured,
+        "variants": variants,
         "calibration": {"copy_bytes": copy_bytes},
         "kernels": kernels,
     }

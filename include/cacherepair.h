@@ -10,8 +10,11 @@
  * where h^B is the output of B Repair Blocks over the fused stale features
  * and token embeddings (paper Section 4.1, "StaleEncoder and token fusion",
  * "Repair Blocks and stale-feature reinjection", "KV residual output and
- * global RoPE").  The add is done in place in the caller's cache.  Global
- * RoPE of the repaired K is not applied: the cache stays canonical.
+ * global RoPE").  The add is done in place in the caller's cache.  cr_repair
+ * leaves K canonical; cr_repair_ex can place the repaired keys at their
+ * global positions in the same pass and runs the paper's controlled
+ * variants (attention topologies, entrance-only features, direct prediction,
+ * output choices).
  *
  * Conventions shared by every entry point:
  *  - Plain C: no C++ or torch types.  All sizes are element counts unless the
@@ -195,6 +198,120 @@ CR_API cr_status cr_repair(void* kv, const cr_kv_layout* layout,
                     const void* token_embeds, const cr_dims* dims,
                     const void* prepared, uint64_t prepared_bytes,
                     void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Variants of the repair forward pass and global placement of the keys.
+ *
+ * Attention topology of the repair blocks (paper appendix "Attention
+ * Topology and Within-Chunk Context"; every topology only allows keys of the
+ * query's own request):
+ *   CR_MASK_BLOCK_CAUSAL    A0, the method: c(j) <= c(i)
+ *   CR_MASK_TOKEN_CAUSAL    A1: j <= i
+ *   CR_MASK_BIDIRECTIONAL   A2: every token of the request
+ *   CR_MASK_BLOCK_DIAGONAL  A3: c(j) == c(i)
+ * Output components that receive the network's correction (Table
+ * tab:repair-components; the network runs in full in every case):
+ *   CR_APPLY_KV (the method), CR_APPLY_K, CR_APPLY_V.
+ */
+enum {
+    CR_MASK_BLOCK_CAUSAL = 0,
+    CR_MASK_TOKEN_CAUSAL = 1,
+    CR_MASK_BIDIRECTIONAL = 2,
+    CR_MASK_BLOCK_DIAGONAL = 3
+};
+enum { CR_APPLY_KV = 0, CR_APPLY_K = 1, CR_APPLY_V = 2 };
+
+/*
+ * The target model's rotary encoding R_M (paper Section 4.1, "Chunk-cache
+ * preparation" and "KV residual output and global RoPE").  Every K head is
+ * rotated in rotate-half pairs (i, i + head_dim/2) by the angle p * f_i, and
+ * both rotated values are multiplied by scale:
+ *   k'_i          = scale * ( k_i cos(p f_i) - k_{i+d/2} sin(p f_i) )
+ *   k'_{i+d/2}    = scale * ( k_{i+d/2} cos(p f_i) + k_i sin(p f_i) )
+ * f_i = theta^(-2i/head_dim) when inv_freq is NULL; otherwise inv_freq is a
+ * host array of head_dim/2 frequencies (radians per position), which covers
+ * the models' frequency-scaling rules.  scale is 1 for plain RoPE.  Angles
+ * and their cosines are evaluated in fp64.
+ */
+typedef struct {
+    double theta;              /* > 0; used when inv_freq is NULL           */
+    const float* inv_freq;     /* host, head_dim/2 entries, or NULL         */
+    float scale;               /* > 0                                       */
+} cr_rope;
+
+/*
+ * Options of cr_repair_ex.  cr_default_options gives the method:
+ * block-causal mask, per-block reinjection, residual output on K and V,
+ * canonical keys.
+ *  mask:             CR_MASK_*.
+ *  reinject:         1 = every block adds P_b(s) + b_b (the method); 0 =
+ *                    variant A4, stale features enter only through token
+ *                    fusion (the blob keeps its w_inj/b_inj entries, unused).
+ *  residual:         1 = KV_hat = KV_stale + sigma_delta * z (the method);
+ *                    0 = variant A5, direct prediction with zero output
+ *                    offset, KV_hat = sigma_delta * z.
+ *  apply:            CR_APPLY_*: components that receive the output; the
+ *                    others keep their stale values.
+ *  keep_first_chunk: 1 = the tokens of the first chunk of every request
+ *                    (chunk index request_chunks[r]) keep their stale values.
+ *  global_rope:      NULL = keys stay canonical (the method as cr_repair
+ *                    computes it); otherwise, after the output add, every key
+ *                    of token t is placed at its global request position,
+ *                    K_hat_t = R_M(p_t) K_hat_t^c, fused into the output add.
+ *                    Requires head_dim <= 128.
+ *  position_offset:  host, n_requests entries (NULL = all 0): global position
+ *                    of the first document token of each request (e.g. the
+ *                    length of a cached preamble); p_t = position_offset[r] +
+ *                    position of t within its request.  Each p_t must be
+ *                    non-negative and below 2^31 - 1.
+ */
+typedef struct {
+    int32_t mask;
+    int32_t reinject;
+    int32_t residual;
+    int32_t apply;
+    int32_t keep_first_chunk;
+    const cr_rope* global_rope;
+    const int32_t* position_offset;
+} cr_options;
+
+/* Fills opt with the method's options. */
+CR_API void cr_default_options(cr_options* opt);
+
+/*
+ * cr_repair with options (see cr_options); cr_repair(...) is
+ * cr_repair_ex(..., &defaults).  Same buffers, errors and asynchrony as
+ * cr_repair; options outside their ranges, a NULL/invalid global_rope field
+ * or head_dim > 128 with global_rope give CR_ERR_DIMS, offsets that put a
+ * position outside [0, 2^31 - 1) give CR_ERR_OFFSETS.
+ */
+CR_API cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout,
+                       const int32_t* chunk_offsets, int32_t n_chunks,
+                       const int32_t* request_chunks, int32_t n_requests,
+                       const void* token_embeds, const cr_dims* dims,
+                       const void* prepared, uint64_t prepared_bytes,
+                       void* workspace, uint64_t workspace_bytes, void* stream,
+                       const cr_options* options);
+
+/*
+ * Rotates every key of tokens [0, N) of a cache in place by R_M(p_t)
+ * (inverse = 0) or R_M(p_t)^-1 (inverse = 1), with p_t as in cr_options
+ * (position within the request plus position_offset[r]); V is not touched.
+ * inverse = 1 with one chunk per request turns independently prefilled
+ * chunk caches into canonical coordinates (paper Section 4.1, "Chunk-cache
+ * preparation"); inverse = 0 places canonical keys at global positions.
+ * kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests: as
+ * cr_repair.  workspace: device, at least cr_rotate_workspace_bytes bytes,
+ * 256-byte aligned.  Requires head_dim <= 256.  Errors as cr_repair_ex.
+ */
+CR_API cr_status cr_rotate_workspace_bytes(const cr_kv_layout* layout, int64_t n_tokens,
+                                    uint64_t* bytes);
+CR_API cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout,
+                         const int32_t* chunk_offsets, int32_t n_chunks,
+                         const int32_t* request_chunks, int32_t n_requests,
+                         const cr_rope* rope, const int32_t* position_offset,
+                         int32_t inverse, void* workspace, uint64_t workspace_bytes,
+                         void* stream);
 
 /*
  * Debug view into the workspace after a cr_repair call that has completed:

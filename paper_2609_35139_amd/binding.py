@@ -29,7 +29,10 @@ STATUS = {
 }
 EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_bytes",
            "cr_prepare_weights", "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair",
+           "cr_default_options", "cr_repair_ex", "cr_rotate_workspace_bytes", "cr_rotate_keys",
            "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]
+CR_MASK = {"block_causal": 0, "token_causal": 1, "bidirectional": 2, "block_diagonal": 3}
+CR_APPLY = {"kv": 0, "k": 1, "v": 2}
 
 
 class CrError(RuntimeError):
@@ -49,6 +52,16 @@ class cr_dims(ctypes.Structure):
     _fields_ = [("d_model", c_int32), ("d_seg", c_int32), ("d_c", c_int32), ("d_b", c_int32),
                 ("n_blocks", c_int32), ("n_heads", c_int32), ("ffn_mult", c_int32),
                 ("rope_theta", c_float), ("ln_eps", c_float)]
+
+
+class cr_rope(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_double), ("inv_freq", POINTER(c_float)), ("scale", c_float)]
+
+
+class cr_options(ctypes.Structure):
+    _fields_ = [("mask", c_int32), ("reinject", c_int32), ("residual", c_int32),
+                ("apply", c_int32), ("keep_first_chunk", c_int32),
+                ("global_rope", POINTER(cr_rope)), ("position_offset", POINTER(c_int32))]
 
 
 class cr_kernel_stat(ctypes.Structure):
@@ -87,12 +100,20 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cr_repair.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
                               c_int32, c_void_p, P(cr_dims), c_void_p, c_uint64, c_void_p,
                               c_uint64, c_void_p]
+    lib.cr_default_options.restype = None
+    lib.cr_default_options.argtypes = [P(cr_options)]
+    lib.cr_repair_ex.argtypes = lib.cr_repair.argtypes + [P(cr_options)]
+    lib.cr_rotate_workspace_bytes.argtypes = [P(cr_kv_layout), c_int64, P(c_uint64)]
+    lib.cr_rotate_keys.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
+                                   c_int32, P(cr_rope), P(c_int32), c_int32, c_void_p, c_uint64,
+                                   c_void_p]
     lib.cr_workspace_view.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, c_char_p,
                                       P(c_uint64), P(c_int64)]
     lib.cr_profile_enable.argtypes = [c_int32]
     lib.cr_profile_read.argtypes = [P(cr_kernel_stat), c_int32, P(c_int32)]
     for name in ["cr_weights_layout", "cr_prepared_bytes", "cr_prepare_weights",
-                 "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_workspace_view",
+                 "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_repair_ex",
+                 "cr_rotate_workspace_bytes", "cr_rotate_keys", "cr_workspace_view",
                  "cr_profile_enable", "cr_profile_read"]:
         getattr(lib, name).restype = c_int32
     _lib = lib
@@ -178,6 +199,92 @@ def cr_repair(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
         req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r,
         token_embeds, ctypes.byref(dims), prepared, prepared_bytes, workspace, workspace_bytes,
         stream), "cr_repair")
+
+
+class Options:
+    """Python view of cr_options (the defaults are the method).
+
+    mask: "block_causal" | "token_causal" | "bidirectional" | "block_diagonal";
+    apply: "kv" | "k" | "v"; global_rope: None or dict(theta=..., inv_freq=[...]
+    or None, scale=1.0); position_offset: None or one int per request.
+    """
+
+    def __init__(self, mask="block_causal", reinject=True, residual=True, apply="kv",
+                 keep_first_chunk=False, global_rope=None, position_offset=None):
+        self.mask, self.reinject, self.residual = mask, reinject, residual
+        self.apply, self.keep_first_chunk = apply, keep_first_chunk
+        self.global_rope, self.position_offset = global_rope, position_offset
+
+    def to_c(self):
+        """(cr_options, keep-alive list) for one call."""
+        o = cr_options()
+        load().cr_default_options(ctypes.byref(o))
+        o.mask = CR_MASK[self.mask] if isinstance(self.mask, str) else int(self.mask)
+        o.reinject = int(self.reinject)
+        o.residual = int(self.residual)
+        o.apply = CR_APPLY[self.apply] if isinstance(self.apply, str) else int(self.apply)
+        o.keep_first_chunk = int(self.keep_first_chunk)
+        keep = []
+        if self.global_rope is not None:
+            r, k = rope_struct(**self.global_rope)
+            keep += [r, k]
+            o.global_rope = ctypes.pointer(r)
+        if self.position_offset is not None:
+            po = np.ascontiguousarray(self.position_offset, dtype=np.int32)
+            keep.append(po)
+            o.position_offset = po.ctypes.data_as(POINTER(c_int32))
+        keep.append(o)
+        return o, keep
+
+
+def rope_struct(theta=1e4, inv_freq=None, scale=1.0):
+    """(cr_rope, keep-alive) for a target rotary encoding."""
+    r = cr_rope()
+    r.theta = float(theta)
+    r.scale = float(scale)
+    keep = None
+    if inv_freq is not None:
+        keep = np.ascontiguousarray(inv_freq, dtype=np.float32)
+        r.inv_freq = keep.ctypes.data_as(POINTER(c_float))
+    return r, keep
+
+
+def cr_repair_ex(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
+                 request_chunks: Optional[Sequence[int]], token_embeds: int, dims: cr_dims,
+                 prepared: int, prepared_bytes: int, workspace: int, workspace_bytes: int,
+                 stream: Optional[int] = None, options: Optional[Options] = None) -> None:
+    off, m = _i32(chunk_offsets)
+    req, r = _i32(request_chunks)
+    o, keep = (options or Options()).to_c()
+    _check(load().cr_repair_ex(
+        kv, ctypes.byref(layout), off.ctypes.data_as(POINTER(c_int32)), m,
+        req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r,
+        token_embeds, ctypes.byref(dims), prepared, prepared_bytes, workspace, workspace_bytes,
+        stream, ctypes.byref(o)), "cr_repair_ex")
+    del keep
+
+
+def cr_rotate_workspace_bytes(layout: cr_kv_layout, n_tokens: int) -> int:
+    b = c_uint64(0)
+    _check(load().cr_rotate_workspace_bytes(ctypes.byref(layout), n_tokens, ctypes.byref(b)),
+           "cr_rotate_workspace_bytes")
+    return b.value
+
+
+def cr_rotate_keys(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
+                   request_chunks: Optional[Sequence[int]], rope: dict,
+                   position_offset: Optional[Sequence[int]], inverse: bool, workspace: int,
+                   workspace_bytes: int, stream: Optional[int] = None) -> None:
+    off, m = _i32(chunk_offsets)
+    req, r = _i32(request_chunks)
+    rs, keep = rope_struct(**rope)
+    po = None if position_offset is None else np.ascontiguousarray(position_offset, np.int32)
+    _check(load().cr_rotate_keys(
+        kv, ctypes.byref(layout), off.ctypes.data_as(POINTER(c_int32)), m,
+        req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r, ctypes.byref(rs),
+        po.ctypes.data_as(POINTER(c_int32)) if po is not None else None, int(inverse),
+        workspace, workspace_bytes, stream), "cr_rotate_keys")
+    del keep
 
 
 def cr_workspace_view(dims: cr_dims, layout: cr_kv_layout, n_tokens: int,

@@ -3,6 +3,7 @@
 #include "../../include/cacherepair.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -101,6 +102,40 @@ cr_status check_offsets(const int32_t* off, int32_t n_chunks, const int32_t* req
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Target rotary encoding: frequencies in fp64 from theta or the caller's
+// table.  Returns CR_ERR_DIMS for a non-finite or non-positive field.
+cr_status key_rope_of(const cr_rope* r, int head_dim, cr::KeyRope* kr) {
+  if (!r || head_dim / 2 > 128) return CR_ERR_DIMS;
+  if (!(r->scale > 0.f) || !std::isfinite(r->scale)) return CR_ERR_DIMS;
+  kr->half = head_dim / 2;
+  kr->scale = r->scale;
+  for (int i = 0; i < kr->half; ++i) {
+    double f;
+    if (r->inv_freq) {
+      f = r->inv_freq[i];
+    } else {
+      if (!(r->theta > 0.0) || !std::isfinite(r->theta)) return CR_ERR_DIMS;
+      f = std::pow(r->theta, -2.0 * i / (double)head_dim);
+    }
+    if (!std::isfinite(f)) return CR_ERR_DIMS;
+    kr->f[i] = f;
+  }
+  return CR_OK;
+}
+
+// Global positions p_t = position_offset[r] + (t - first token of r) must lie
+// in [0, 2^31 - 1).
+cr_status check_positions(const int32_t* off, int32_t n_chunks, const int32_t* req,
+                          int32_t n_req, const int32_t* pos_offset) {
+  const int nr = req ? n_req : 1;
+  for (int r = 0; r < nr; ++r) {
+    const int64_t o = pos_offset ? pos_offset[r] : 0;
+    const int64_t len = req ? (int64_t)off[req[r + 1]] - off[req[r]] : off[n_chunks];
+    if (o < 0 || o + len >= ((int64_t)1 << 31) - 1) return CR_ERR_OFFSETS;
+  }
+  return CR_OK;
+}
 
 cr_status check_device() {
   static int ok[64] = {0};  // 0 unknown, 1 gfx950, -1 not
@@ -206,7 +241,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
 
 struct Workspace {
   int64_t n, n_pad, ldst, ldinj;
-  uint64_t lo, hi, pos, rope, U, st, inj, h, a, q, k, vt, o, f, total;
+  uint64_t lo, hi, pos, gpos, flags, rope, krope, U, st, inj, h, a, q, k, vt, o, f, total;
 };
 
 Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
@@ -221,7 +256,9 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.ldinj = (int64_t)d->n_blocks * db;
   Arena a;
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
+  w.gpos = a.take(N * 4); w.flags = a.take(N * 4);
   w.rope = a.take(std::max<int64_t>(N, 1) * (dhd / 2) * 8);
+  w.krope = a.take(N * (l->head_dim / 2) * 8);        // global key placement table
   w.U = a.take(N * kc_pad * T);
   w.st = a.take(N * w.ldst * T);
   w.inj = a.take(N * w.ldinj * T);
@@ -344,10 +381,22 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
   return CR_OK;
 }
 
+// Options of one call, validated.
+struct CallOpts {
+  int mask = CR_MASK_BLOCK_CAUSAL;
+  bool reinject = true;
+  int expand_mode = cr::EXPAND_RESIDUAL | cr::EXPAND_K | cr::EXPAND_V;
+  bool keep_first = false;
+  bool place_keys = false;
+  cr::KeyRope kr{};
+  const int32_t* pos_offset = nullptr;
+};
+
 template <typename T>
 cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t n_chunks,
                       const int32_t* req, int32_t n_req, const T* emb, const cr_dims* d,
-                      const char* prep, char* ws, int64_t N, int max_len, hipStream_t s) {
+                      const char* prep, char* ws, int64_t N, int max_len, const CallOpts& opt,
+                      hipStream_t s) {
   const Prepared P = prepared_layout(d, l);
   const Workspace W = workspace_layout(d, l, N);
   const int M = (int)N;
@@ -361,7 +410,10 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   int* lo = reinterpret_cast<int*>(ws + W.lo);
   int* hi = reinterpret_cast<int*>(ws + W.hi);
   int* pos = reinterpret_cast<int*>(ws + W.pos);
+  int* gpos = opt.place_keys ? reinterpret_cast<int*>(ws + W.gpos) : nullptr;
+  int* flags = opt.keep_first ? reinterpret_cast<int*>(ws + W.flags) : nullptr;
   float2* rope = reinterpret_cast<float2*>(ws + W.rope);
+  float2* krope = reinterpret_cast<float2*>(ws + W.krope);
   T *U = WT(W.U), *st = WT(W.st), *inj = WT(W.inj), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q),
     *k = WT(W.k), *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
   const int64_t ldinj = W.ldinj;
@@ -371,9 +423,13 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   const float eps = d->ln_eps;
 
   CR_TRY(timed("schedule", s, [&] {
-      return cr::chunk_schedule(off, n_chunks, req, n_req, lo, hi, pos, s); }));
+      return cr::chunk_schedule(off, n_chunks, req, n_req, opt.mask, opt.pos_offset, lo, hi, pos,
+                                gpos, flags, s); }));
   CR_TRY(timed("rope_table", s, [&] {
       return cr::rope_table(rope, max_len, dhd, (double)d->rope_theta, s); }));
+  if (opt.place_keys)
+    CR_TRY(timed("key_rope_table", s, [&] {
+        return cr::key_rope_table(krope, gpos, M, opt.kr, s); }));
   // StaleEncoder: per-segment projections, compression, LN_enc -> s = st[:, :d_c]
   CR_TRY(timed("compress_segments", s, [&] {
       return cr::compress_segments<T>(kv, ks, l->n_layers, PT(P.w_seg), PF(P.b_seg), U, P.kc_pad,
@@ -384,7 +440,9 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   CR_TRY(timed("layernorm", s, [&] {
       return cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s); }));
   // reinjection P_b(s) + b_b of every block at once -> inj[:, b*d_b : (b+1)*d_b]
-  if (B > 0)
+  // (none for the entrance-only variant)
+  const bool rj = opt.reinject && B > 0;
+  if (rj)
     CR_TRY(timed("gemm_inject", s, [&] {
         return cr::gemm_bias<T>(st, ldst, PT(P.w_inj), dc, M, B * db, dc, inj, ldinj,
                                 PF(P.b_inj), nullptr, 0, false, s); }));
@@ -394,11 +452,11 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
                           0, false, s); }));
   CR_TRY(timed("gemm_fuse", s, [&] {
       return cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
-                          B > 0 ? inj : nullptr, ldinj, false, s); }));
+                          rj ? inj : nullptr, ldinj, false, s); }));
   // h holds x_b = h^{b-1} + P_b(s) on entry to block b, h^B after the last block
   for (int b = 0; b < B; ++b) {
     const BlockP& Bk = P.blk[b];
-    const T* next_inj = b + 1 < B ? inj + (int64_t)(b + 1) * db : nullptr;
+    const T* next_inj = rj && b + 1 < B ? inj + (int64_t)(b + 1) * db : nullptr;
     CR_TRY(timed("layernorm", s, [&] {
         return cr::layernorm<T>(h, db, a, db, PF(Bk.ln1_g), PF(Bk.ln1_b), M, db, eps, s); }));
     CR_TRY(timed("gemm_qkv", s, [&] {
@@ -421,7 +479,8 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
       return cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s); }));
   CR_TRY(timed("gemm_expand", s, [&] {
       return cr::gemm_expand<T>(a, db, PT(P.w_out), M, D, db, kv, ks, PF(P.b_out),
-                            PF(P.sigma_delta), s); }));
+                            PF(P.sigma_delta), opt.expand_mode, flags,
+                            opt.place_keys ? krope : nullptr, s); }));
   return CR_OK;
 }
 
@@ -535,22 +594,58 @@ cr_status cr_chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
   st = check_device();
   if (st != CR_OK) return st;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (cr::chunk_schedule(chunk_offsets, n_chunks, request_chunks, n_requests, rows, rows + N,
-                         rows + 2 * N, s) != hipSuccess)
+  if (cr::chunk_schedule(chunk_offsets, n_chunks, request_chunks, n_requests,
+                         CR_MASK_BLOCK_CAUSAL, nullptr, rows, rows + N, rows + 2 * N, nullptr,
+                         nullptr, s) != hipSuccess)
     return CR_ERR_LAUNCH;
   return CR_OK;
 }
 
-cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
-                    int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
-                    const void* token_embeds, const cr_dims* dims, const void* prepared,
-                    uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
-                    void* stream) {
-  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace) return CR_ERR_NULL;
+void cr_default_options(cr_options* opt) {
+  if (!opt) return;
+  std::memset(opt, 0, sizeof(*opt));
+  opt->mask = CR_MASK_BLOCK_CAUSAL;
+  opt->reinject = 1;
+  opt->residual = 1;
+  opt->apply = CR_APPLY_KV;
+  opt->keep_first_chunk = 0;
+  opt->global_rope = nullptr;
+  opt->position_offset = nullptr;
+}
+
+cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                       int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                       const void* token_embeds, const cr_dims* dims, const void* prepared,
+                       uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
+                       void* stream, const cr_options* options) {
+  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace || !options)
+    return CR_ERR_NULL;
   cr_status st = check_dims(dims, layout);
   if (st != CR_OK) return st;
   st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
   if (st != CR_OK) return st;
+  const cr_options& o = *options;
+  CallOpts opt;
+  if (o.mask < CR_MASK_BLOCK_CAUSAL || o.mask > CR_MASK_BLOCK_DIAGONAL) return CR_ERR_DIMS;
+  if ((o.reinject != 0 && o.reinject != 1) || (o.residual != 0 && o.residual != 1) ||
+      (o.keep_first_chunk != 0 && o.keep_first_chunk != 1))
+    return CR_ERR_DIMS;
+  if (o.apply < CR_APPLY_KV || o.apply > CR_APPLY_V) return CR_ERR_DIMS;
+  opt.mask = o.mask;
+  opt.reinject = o.reinject == 1;
+  opt.expand_mode = (o.residual ? cr::EXPAND_RESIDUAL : 0) |
+                    (o.apply != CR_APPLY_V ? cr::EXPAND_K : 0) |
+                    (o.apply != CR_APPLY_K ? cr::EXPAND_V : 0);
+  opt.keep_first = o.keep_first_chunk == 1;
+  if (o.global_rope) {
+    if (layout->head_dim > 128) return CR_ERR_DIMS;
+    st = key_rope_of(o.global_rope, layout->head_dim, &opt.kr);
+    if (st != CR_OK) return st;
+    st = check_positions(chunk_offsets, n_chunks, request_chunks, n_requests, o.position_offset);
+    if (st != CR_OK) return st;
+    opt.place_keys = true;
+    opt.pos_offset = o.position_offset;
+  }
   const int64_t N = chunk_offsets[n_chunks];
   if (N >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
   st = check_layout(layout, N);
@@ -576,11 +671,84 @@ cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_o
     return repair_impl<bf16>(static_cast<bf16*>(kv), layout, chunk_offsets, n_chunks,
                              request_chunks, n_requests, static_cast<const bf16*>(token_embeds),
                              dims, static_cast<const char*>(prepared),
-                             static_cast<char*>(workspace), N, max_len, s);
+                             static_cast<char*>(workspace), N, max_len, opt, s);
   return repair_impl<float>(static_cast<float*>(kv), layout, chunk_offsets, n_chunks,
                             request_chunks, n_requests, static_cast<const float*>(token_embeds),
                             dims, static_cast<const char*>(prepared),
-                            static_cast<char*>(workspace), N, max_len, s);
+                            static_cast<char*>(workspace), N, max_len, opt, s);
+}
+
+cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                    int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                    const void* token_embeds, const cr_dims* dims, const void* prepared,
+                    uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
+                    void* stream) {
+  cr_options o;
+  cr_default_options(&o);
+  return cr_repair_ex(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
+                      token_embeds, dims, prepared, prepared_bytes, workspace, workspace_bytes,
+                      stream, &o);
+}
+
+// workspace of cr_rotate_keys: lo, hi, pos, gpos (int32 each) and the table
+static uint64_t rotate_ws_bytes(const cr_kv_layout* l, int64_t N) {
+  return align_up(4 * (uint64_t)N * 4) + align_up((uint64_t)N * (l->head_dim / 2) * 8);
+}
+
+cr_status cr_rotate_workspace_bytes(const cr_kv_layout* layout, int64_t n_tokens,
+                                    uint64_t* bytes) {
+  if (!layout || !bytes) return CR_ERR_NULL;
+  if (n_tokens < 0 || n_tokens >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  if (layout->head_dim < 32 || layout->head_dim > 256 || layout->head_dim % 32) return CR_ERR_DIMS;
+  *bytes = rotate_ws_bytes(layout, n_tokens);
+  return CR_OK;
+}
+
+cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                         int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                         const cr_rope* rope, const int32_t* position_offset, int32_t inverse,
+                         void* workspace, uint64_t workspace_bytes, void* stream) {
+  if (!kv || !layout || !rope || !workspace) return CR_ERR_NULL;
+  if (layout->n_layers < 1 || layout->n_kv_heads < 1 || layout->head_dim < 32 ||
+      layout->head_dim > 256 || layout->head_dim % 32)
+    return CR_ERR_DIMS;
+  if (layout->dtype != CR_DTYPE_BF16 && layout->dtype != CR_DTYPE_F32) return CR_ERR_DTYPE;
+  if (inverse != 0 && inverse != 1) return CR_ERR_DIMS;
+  cr_status st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
+  if (st != CR_OK) return st;
+  cr::KeyRope kr{};
+  st = key_rope_of(rope, layout->head_dim, &kr);
+  if (st != CR_OK) return st;
+  st = check_positions(chunk_offsets, n_chunks, request_chunks, n_requests, position_offset);
+  if (st != CR_OK) return st;
+  const int64_t N = chunk_offsets[n_chunks];
+  if (N >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  st = check_layout(layout, N);
+  if (st != CR_OK) return st;
+  if (!aligned(kv, 16)) return CR_ERR_LAYOUT;
+  if (workspace_bytes < rotate_ws_bytes(layout, N) || !aligned(workspace, ALIGN))
+    return CR_ERR_WORKSPACE;
+  if (N == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  int* rows = static_cast<int*>(workspace);
+  float2* tab = reinterpret_cast<float2*>(static_cast<char*>(workspace) + align_up(4 * (uint64_t)N * 4));
+  const cr::KvStrides ks{layout->stride_layer, layout->stride_kv, layout->stride_token,
+                         layout->stride_head, layout->n_kv_heads, layout->head_dim};
+  if (cr::chunk_schedule(chunk_offsets, n_chunks, request_chunks, n_requests,
+                         CR_MASK_BLOCK_CAUSAL, position_offset, rows, rows + N, rows + 2 * N,
+                         rows + 3 * N, nullptr, s) != hipSuccess)
+    return CR_ERR_LAUNCH;
+  if (cr::key_rope_table(tab, rows + 3 * N, (int)N, kr, s) != hipSuccess) return CR_ERR_LAUNCH;
+  hipError_t e;
+  if (layout->dtype == CR_DTYPE_BF16)
+    e = cr::rotate_keys<bf16>(static_cast<bf16*>(kv), ks, layout->n_layers, (int)N, tab,
+                              inverse == 1, rope->scale, s);
+  else
+    e = cr::rotate_keys<float>(static_cast<float*>(kv), ks, layout->n_layers, (int)N, tab,
+                               inverse == 1, rope->scale, s);
+  return e == hipSuccess ? CR_OK : CR_ERR_LAUNCH;
 }
 
 cr_status cr_profile_enable(int32_t max_launches) {

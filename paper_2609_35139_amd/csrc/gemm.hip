@@ -60,6 +60,7 @@ __device__ __forceinline__ void load8f(const float* p, float* v) {
 
 template <typename T>
 struct EpiBias {
+  static constexpr bool kFullTile = false;
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
   int64_t ldr2; int gelu;
   template <int ROWS, int COLS, int LDC>
@@ -112,6 +113,7 @@ struct EpiBias {
 
 template <typename T>
 struct EpiQKV {
+  static constexpr bool kFullTile = false;
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
   template <int ROWS, int COLS, int LDC>
@@ -176,41 +178,138 @@ struct EpiQKV {
   }
 };
 
+// Coordinate j = ((l*2 + kv)*H + h)*d_h + i of the residual in the strided
+// cache: pointer of token 0's element, and whether it is a K coordinate.
+template <typename T>
+__device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* is_k) {
+  const int i = j % ks.head_dim;
+  const int seg = j / ks.head_dim;
+  const int h = seg % ks.n_kv_heads;
+  const int lk = seg / ks.n_kv_heads;
+  *is_k = (lk & 1) == 0;
+  return kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv + (int64_t)h * ks.head + i;
+}
+
 template <typename T>
 struct EpiExpand {
-  T* kv; KvStrides ks; const float* bias; const float* sigma;
+  static constexpr bool kFullTile = false;
+  T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   template <int ROWS, int COLS, int LDC>
   __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS>;
     const int c = S::col(), gn = n0 + c;
     if (gn >= N) return;
-    // coordinate j = ((l*2 + kv)*H + h)*d_h + i; 8 | d_h keeps a segment in one head
-    const int i = gn % ks.head_dim;
-    const int seg = gn / ks.head_dim;
-    const int h = seg % ks.n_kv_heads;
-    const int lk = seg / ks.n_kv_heads;
-    T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
-              (int64_t)h * ks.head + i;
+    // 8 | d_h keeps a segment in one head
+    bool is_k;
+    T* base = kv_coord(kv, ks, gn, &is_k);
+    if (!(mode & (is_k ? EXPAND_K : EXPAND_V))) return;   // component left stale
+    const bool res = mode & EXPAND_RESIDUAL;
     float b[8], sg[8];
     load8f(bias + gn, b);
     load8f(sigma + gn, sg);
     Vec8<T> x[S::PASSES];
+    int kp[S::PASSES];
 #pragma unroll
     for (int p = 0; p < S::PASSES; ++p) {
       const int gm = m0 + S::row(p);
-      if (gm < M) x[p].load(base + (int64_t)gm * ks.token);
+      kp[p] = (gm < M && keep) ? keep[gm] : 0;
+      if (gm < M && res) x[p].load(base + (int64_t)gm * ks.token);
     }
 #pragma unroll
     for (int p = 0; p < S::PASSES; ++p) {
       const int r = S::row(p), gm = m0 + r;
-      if (gm >= M) continue;
+      if (gm >= M || kp[p]) continue;
       float a[8], f[8];
       load8f(Cs + r * LDC + c, a);
-      x[p].to_float(f);
+      if (res) x[p].to_float(f);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = f[e] + sg[e] * (a[e] + b[e]);
+      for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + sg[e] * (a[e] + b[e]);
       x[p].from_float(f);
       x[p].store(base + (int64_t)gm * ks.token);
+    }
+  }
+};
+
+// Output add followed by the target model's rotation of every key head
+// (global placement), on a fully staged tile: a thread owns 8 rotate-half
+// pairs (columns c .. c+7 and c+half .. c+half+7 of one head) of a set of
+// rows, so both members of every pair are rotated in registers.  Requires
+// head_dim <= 128 (a head never straddles two 128-column tiles).
+template <typename T>
+struct EpiExpandRope {
+  static constexpr bool kFullTile = true;
+  T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
+  const float2* rope;   // [M][head_dim/2] scaled (cos, sin)
+  template <int ROWS, int COLS, int LDC>
+  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+    constexpr int PAIRS = COLS / 16;               // 8-pair groups per tile row
+    constexpr int RSTEP = 256 / PAIRS, PASSES = ROWS / RSTEP;
+    const int dh = ks.head_dim, half = dh / 2, sph = half / 8;
+    const int p = threadIdx.x % PAIRS;
+    const int c1 = (p / sph) * dh + (p % sph) * 8, c2 = c1 + half;
+    const int g1 = n0 + c1, g2 = n0 + c2;
+    if (g2 >= N) return;
+    bool is_k;
+    T* b1 = kv_coord(kv, ks, g1, &is_k);
+    T* b2 = b1 + half;
+    const int i0 = g1 % dh;
+    const bool on = mode & (is_k ? EXPAND_K : EXPAND_V);
+    if (!on && !is_k) return;                      // stale V: nothing to write
+    const bool res = mode & EXPAND_RESIDUAL;
+    float bb1[8], bb2[8], s1[8], s2[8];
+    load8f(bias + g1, bb1); load8f(bias + g2, bb2);
+    load8f(sigma + g1, s1); load8f(sigma + g2, s2);
+    Vec8<T> x1[PASSES], x2[PASSES];
+    int kp[PASSES];
+    float4 cs[PASSES][4];
+#pragma unroll
+    for (int q = 0; q < PASSES; ++q) {
+      const int gm = m0 + threadIdx.x / PAIRS + q * RSTEP;
+      kp[q] = (gm < M && keep) ? keep[gm] : 0;
+      if (gm < M) {
+        x1[q].load(b1 + (int64_t)gm * ks.token);
+        x2[q].load(b2 + (int64_t)gm * ks.token);
+        if (is_k) {
+          const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)gm * half + i0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < PASSES; ++q) {
+      const int r = threadIdx.x / PAIRS + q * RSTEP, gm = m0 + r;
+      if (gm >= M) continue;
+      float y1[8], y2[8];
+      x1[q].to_float(y1);
+      x2[q].to_float(y2);
+      if (on && !kp[q]) {
+        float a1[8], a2[8];
+        load8f(Cs + r * LDC + c1, a1);
+        load8f(Cs + r * LDC + c2, a2);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          y1[e] = (res ? y1[e] : 0.f) + s1[e] * (a1[e] + bb1[e]);
+          y2[e] = (res ? y2[e] : 0.f) + s2[e] * (a2[e] + bb2[e]);
+        }
+      } else if (!is_k) {
+        continue;
+      }
+      if (is_k) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
+          const float u0 = y1[2 * e], v0 = y2[2 * e], u1 = y1[2 * e + 1], v1 = y2[2 * e + 1];
+          y1[2 * e] = t.x * u0 - t.y * v0;
+          y2[2 * e] = t.x * v0 + t.y * u0;
+          y1[2 * e + 1] = t.z * u1 - t.w * v1;
+          y2[2 * e + 1] = t.z * v1 + t.w * u1;
+        }
+      }
+      x1[q].from_float(y1);
+      x2[q].from_float(y2);
+      x1[q].store(b1 + (int64_t)gm * ks.token);
+      x2[q].store(b2 + (int64_t)gm * ks.token);
     }
   }
 };
@@ -231,7 +330,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
                                                       int M, int N, int K, Epi epi) {
   using MM = Mma32<T>;
   using frag = typename MM::frag;
-  __shared__ __align__(1024) char smem[G::LDS];
+  constexpr int LDCF = G::BN + 4;                    // full-tile staging row
+  constexpr size_t LDS_FULL = Epi::kFullTile ? (size_t)G::BM * LDCF * sizeof(float) : 0;
+  __shared__ __align__(1024) char smem[G::LDS > LDS_FULL ? G::LDS : LDS_FULL];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.y * G::BM, n0 = blockIdx.x * G::BN;
@@ -307,6 +408,21 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
   // v holds row (v/4)*8 + (lane/32)*4 + v%4), then all threads run the
   // epilogue on that half.
   float* Cs = reinterpret_cast<float*>(smem);
+  if constexpr (Epi::kFullTile) {
+    // epilogues that pair columns across the two halves see the whole tile
+    __syncthreads();  // ring no longer read
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          Cs[(wm + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * LDCF + wn + j * 32 + fr] =
+              acc[i][j][v];
+    __syncthreads();
+    epi.template run<G::BM, G::BN, LDCF>(Cs, m0, n0, M, N);
+    return;
+  }
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     __syncthreads();  // ring (or the previous half) no longer read
@@ -366,8 +482,14 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
 
 template <typename T>
 hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K, T* kv,
-                       KvStrides ks, const float* bias, const float* sigma, hipStream_t s) {
-  EpiExpand<T> e{kv, ks, bias, sigma};
+                       KvStrides ks, const float* bias, const float* sigma, int mode,
+                       const int* keep, const float2* key_rope, hipStream_t s) {
+  if (key_rope) {
+    if (ks.head_dim > 128) return hipErrorInvalidValue;
+    EpiExpandRope<T> e{kv, ks, bias, sigma, mode, keep, key_rope};
+    return launch<T>(A, lda, B, K, M, N, K, e, s);
+  }
+  EpiExpand<T> e{kv, ks, bias, sigma, mode, keep};
   return launch<T>(A, lda, B, K, M, N, K, e, s);
 }
 
@@ -378,7 +500,8 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*, \
                                   int64_t, const float*, const int*, const float2*, hipStream_t); \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides, \
-                                     const float*, const float*, hipStream_t);
+                                     const float*, const float*, int, const int*,               \
+                                     const float2*, hipStream_t);
 CR_INST(bf16)
 CR_INST(float)
 #undef CR_INST

@@ -47,11 +47,19 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
                     T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
                     const float2* rope, hipStream_t s);
 
-// KV residual head fused with the in-place add into the strided cache:
-// kv[t, j] += sigma[j] * (acc[t, j] + bias[j]) for j in [0, D_KV).
+// KV residual head fused with the output add into the strided cache, for
+// coordinates j in [0, D_KV) of the selected components:
+//   kv[t, j] = (residual ? kv[t, j] : 0) + sigma[j] * (acc[t, j] + bias[j]).
+// mode: EXPAND_RESIDUAL | EXPAND_K | EXPAND_V.  keep (may be null): tokens
+// with keep[t] != 0 are left unchanged.  With key_rope (may be null, table
+// [M][head_dim/2] of scaled (cos, sin), head_dim <= 128) every key head of
+// every token is then rotated by its row of the table, whether or not it
+// received the output.
+enum { EXPAND_RESIDUAL = 1, EXPAND_K = 2, EXPAND_V = 4 };
 template <typename T>
 hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K, T* kv,
-                       KvStrides ks, const float* bias, const float* sigma, hipStream_t s);
+                       KvStrides ks, const float* bias, const float* sigma, int mode,
+                       const int* keep, const float2* key_rope, hipStream_t s);
 
 // ---- block-causal flash attention (per-row key interval [lo, hi)).
 template <typename T>
@@ -70,10 +78,29 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
                              const float* bseg, T* U, int64_t ldu, int d_seg, int N,
                              hipStream_t s);
 
-// ---- chunk schedule: lo/hi/pos per token from host chunk structure.
+// ---- chunk schedule: per token the key interval [lo, hi) of the attention
+// topology `mask` (values of CR_MASK_*), the position within the request and,
+// when the pointers are not null, the global position (position_offset of the
+// request + position; pos_offset may be null = 0) and the first-chunk flag.
 hipError_t chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
-                          const int32_t* request_chunks, int32_t n_requests, int* lo, int* hi,
-                          int* pos, hipStream_t s);
+                          const int32_t* request_chunks, int32_t n_requests, int mask,
+                          const int32_t* pos_offset, int* lo, int* hi, int* pos, int* gpos,
+                          int* flags, hipStream_t s);
+
+// ---- target-model key rotation R_M(p): frequencies of the rotate-half pairs
+// (fp64) and the factor applied to cos and sin.
+struct KeyRope {
+  int half;
+  double scale;
+  double f[128];
+};
+// tab[t][i] = scale * (cos, sin)(gpos[t] * f_i), i < half.
+hipError_t key_rope_table(float2* tab, const int* gpos, int N, const KeyRope& kr, hipStream_t s);
+// Rotates every key head of tokens [0, N) in place by the table (inverse:
+// by the inverse rotation, dividing by scale^2 as well).
+template <typename T>
+hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* tab, bool inverse,
+                       float scale, hipStream_t s);
 
 // ---- RoPE (cos, sin) table for positions [0, max_pos), computed in fp64.
 hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStream_t s);

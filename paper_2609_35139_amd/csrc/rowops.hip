@@ -163,16 +163,26 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
 }
 
 // ---------------------------------------------------------- chunk schedule
-constexpr int SCHED_CHUNKS = 256;
+// Per token t: the key interval [lo, hi) of its attention row under the
+// chosen topology (all of them allow only t's request), its 0-based position
+// within the request, optionally its global position and a flag for the
+// first chunk of its request.  Chunks are passed by value in batches.
+constexpr int SCHED_CHUNKS = 128;
 struct SchedBatch {
-  int count;                      // chunks in this batch
-  int offs[SCHED_CHUNKS + 1];     // token offsets of the batch's chunks
-  int req_start[SCHED_CHUNKS];    // first token of each chunk's request
+  int count;                          // chunks in this batch
+  int mask;                           // topology, values of CR_MASK_*
+  int offs[SCHED_CHUNKS + 1];         // token offsets of the batch's chunks
+  int req_start[SCHED_CHUNKS];        // first token of each chunk's request
+  int req_end[SCHED_CHUNKS];          // one past the request's last token
+  int gbase[SCHED_CHUNKS];            // global position of token t is t + gbase
+  unsigned first[SCHED_CHUNKS / 32];  // bit c: chunk c opens its request
 };
 
 __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __restrict__ lo,
                                                        int* __restrict__ hi,
-                                                       int* __restrict__ pos) {
+                                                       int* __restrict__ pos,
+                                                       int* __restrict__ gpos,
+                                                       int* __restrict__ flags) {
   const int t = sb.offs[0] + blockIdx.x * 256 + threadIdx.x;
   if (t >= sb.offs[sb.count]) return;
   // largest c with offs[c] <= t (skips empty chunks)
@@ -181,33 +191,136 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __res
     const int mid = (a + b) >> 1;
     if (sb.offs[mid] <= t) a = mid; else b = mid;
   }
-  lo[t] = sb.req_start[a];
-  hi[t] = sb.offs[a + 1];
+  int l = sb.req_start[a], h = sb.offs[a + 1];      // block-causal: c(j) <= c(i)
+  if (sb.mask == 1) h = t + 1;                      // token-causal: j <= i
+  else if (sb.mask == 2) h = sb.req_end[a];         // bidirectional
+  else if (sb.mask == 3) l = sb.offs[a];            // block-diagonal: c(j) == c(i)
+  lo[t] = l;
+  hi[t] = h;
   pos[t] = t - sb.req_start[a];
+  if (gpos) gpos[t] = t + sb.gbase[a];
+  if (flags) flags[t] = (sb.first[a >> 5] >> (a & 31)) & 1;
 }
 
 hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* req,
-                          int32_t n_req, int* lo, int* hi, int* pos, hipStream_t s) {
-  std::vector<int> rs(n_chunks);
-  if (req == nullptr) {
-    std::fill(rs.begin(), rs.end(), off[0]);
-  } else {
-    for (int r = 0; r < n_req; ++r)
-      for (int c = req[r]; c < req[r + 1]; ++c) rs[c] = off[req[r]];
+                          int32_t n_req, int mask, const int32_t* pos_offset, int* lo, int* hi,
+                          int* pos, int* gpos, int* flags, hipStream_t s) {
+  std::vector<int> rs(n_chunks), re(n_chunks), gb(n_chunks), first(n_chunks);
+  const int nr = req ? n_req : 1;
+  for (int r = 0; r < nr; ++r) {
+    const int c0 = req ? req[r] : 0, c1 = req ? req[r + 1] : n_chunks;
+    for (int c = c0; c < c1; ++c) {
+      rs[c] = off[c0];
+      re[c] = off[c1];
+      gb[c] = (pos_offset ? pos_offset[r] : 0) - off[c0];
+      first[c] = c == c0;
+    }
   }
   for (int c0 = 0; c0 < n_chunks; c0 += SCHED_CHUNKS) {
     SchedBatch sb;
     sb.count = std::min(SCHED_CHUNKS, n_chunks - c0);
+    sb.mask = mask;
     for (int i = 0; i <= sb.count; ++i) sb.offs[i] = off[c0 + i];
-    for (int i = 0; i < sb.count; ++i) sb.req_start[i] = rs[c0 + i];
+    for (int i = 0; i < SCHED_CHUNKS / 32; ++i) sb.first[i] = 0;
+    for (int i = 0; i < sb.count; ++i) {
+      sb.req_start[i] = rs[c0 + i];
+      sb.req_end[i] = re[c0 + i];
+      sb.gbase[i] = gb[c0 + i];
+      sb.first[i >> 5] |= (unsigned)first[c0 + i] << (i & 31);
+    }
     const int ntok = sb.offs[sb.count] - sb.offs[0];
     if (ntok == 0) continue;
-    CR_LAUNCH(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos);
+    CR_LAUNCH(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos, gpos,
+              flags);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
+
+// ------------------------------------------------- target-model key rotation
+// tab[t][i] = scale * (cos, sin)(gpos[t] * f_i), angles and cosines in fp64.
+__global__ __launch_bounds__(256) void key_rope_table_kernel(float2* __restrict__ tab,
+                                                             const int* __restrict__ gpos, int N,
+                                                             KeyRope kr) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)N * kr.half) return;
+  const int t = (int)(idx / kr.half), i = (int)(idx % kr.half);
+  const double ang = (double)gpos[t] * kr.f[i];
+  tab[idx] = make_float2((float)(kr.scale * cos(ang)), (float)(kr.scale * sin(ang)));
+}
+
+hipError_t key_rope_table(float2* tab, const int* gpos, int N, const KeyRope& kr, hipStream_t s) {
+  const int64_t n = (int64_t)N * kr.half;
+  if (n <= 0) return hipSuccess;
+  CR_LAUNCH(key_rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tab, gpos,
+            N, kr);
+  return hipGetLastError();
+}
+
+// One thread rotates 8 rotate-half pairs (i .. i+7, i+half .. i+half+7) of
+// one key head of one token, with the (scaled) table of its position:
+// forward  k1' = c k1 - s k2,  k2' = c k2 + s k1;
+// inverse  k1' = (c k1 + s k2) / scale^2,  k2' = (c k2 - s k1) / scale^2.
+template <typename T>
+__global__ __launch_bounds__(256) void rotate_keys_kernel(T* __restrict__ kv, KvStrides ks,
+                                                          int n_layers, int N,
+                                                          const float2* __restrict__ tab,
+                                                          int inverse, float inv_scale2) {
+  const int half = ks.head_dim / 2, per_head = half / 8;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t per_tok = (int64_t)n_layers * ks.n_kv_heads * per_head;
+  if (idx >= (int64_t)N * per_tok) return;
+  const int t = (int)(idx / per_tok);
+  int rem = (int)(idx % per_tok);
+  const int seg8 = rem % per_head;
+  rem /= per_head;
+  const int h = rem % ks.n_kv_heads, l = rem / ks.n_kv_heads;
+  const int i0 = seg8 * 8;
+  T* p1 = kv + (int64_t)l * ks.layer + (int64_t)t * ks.token + (int64_t)h * ks.head + i0;
+  T* p2 = p1 + half;
+  Vec8<T> a, b;
+  a.load(p1);
+  b.load(p2);
+  const float4* cs = reinterpret_cast<const float4*>(tab + (int64_t)t * half + i0);
+  float x1[8], x2[8], y1[8], y2[8];
+  a.to_float(x1);
+  b.to_float(x2);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float4 q = cs[e];   // (cos, sin) of pairs 2e and 2e+1
+    const float c[2] = {q.x, q.z}, sn[2] = {q.y, q.w};
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = 2 * e + u;
+      if (inverse) {
+        y1[k] = (c[u] * x1[k] + sn[u] * x2[k]) * inv_scale2;
+        y2[k] = (c[u] * x2[k] - sn[u] * x1[k]) * inv_scale2;
+      } else {
+        y1[k] = c[u] * x1[k] - sn[u] * x2[k];
+        y2[k] = c[u] * x2[k] + sn[u] * x1[k];
+      }
+    }
+  }
+  a.from_float(y1);
+  b.from_float(y2);
+  a.store(p1);
+  b.store(p2);
+}
+
+template <typename T>
+hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* tab, bool inverse,
+                       float scale, hipStream_t s) {
+  const int64_t n = (int64_t)N * n_layers * ks.n_kv_heads * (ks.head_dim / 16);
+  if (n <= 0) return hipSuccess;
+  CR_LAUNCH((rotate_keys_kernel<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, kv, ks,
+            n_layers, N, tab, inverse ? 1 : 0, 1.0f / (scale * scale));
+  return hipGetLastError();
+}
+template hipError_t rotate_keys<bf16>(bf16*, KvStrides, int, int, const float2*, bool, float,
+                                      hipStream_t);
+template hipError_t rotate_keys<float>(float*, KvStrides, int, int, const float2*, bool, float,
+                                       hipStream_t);
 
 // ------------------------------------------------------------ RoPE table
 __global__ __launch_bounds__(256) void rope_table_kernel(float2* tab, int max_pos, int half,

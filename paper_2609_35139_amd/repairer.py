@@ -68,8 +68,11 @@ class Repairer:
                request_chunks: Optional[Sequence[int]], token_embeds: torch.Tensor,
                workspace: Optional[torch.Tensor] = None,
                layout: Optional[B.cr_kv_layout] = None,
-               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-        """Repair ``kv`` in place (layer-major [L][2][N][H][d_h] unless a layout is given)."""
+               stream: Optional[torch.cuda.Stream] = None,
+               options: Optional[B.Options] = None) -> torch.Tensor:
+        """Repair ``kv`` in place (layer-major [L][2][N][H][d_h] unless a layout
+        is given).  options (binding.Options) selects a variant; None is the
+        method (cr_repair)."""
         n = int(chunk_offsets[-1])
         lay = layout if layout is not None else self.layout(n)
         ws = workspace if workspace is not None else self.workspace(n)
@@ -77,7 +80,27 @@ class Repairer:
             raise TypeError("kv and token_embeds must use the repairer's storage dtype")
         if not token_embeds.is_contiguous() or token_embeds.shape != (n, self.dims.d_model):
             raise ValueError("token_embeds must be a contiguous [N, d_model] tensor")
-        B.cr_repair(kv.data_ptr(), lay, chunk_offsets, request_chunks, token_embeds.data_ptr(),
-                    self.dims, self.prepared.data_ptr(), self.prepared_bytes, ws.data_ptr(),
-                    ws.numel(), _stream_handle(stream))
+        if options is None:
+            B.cr_repair(kv.data_ptr(), lay, chunk_offsets, request_chunks,
+                        token_embeds.data_ptr(), self.dims, self.prepared.data_ptr(),
+                        self.prepared_bytes, ws.data_ptr(), ws.numel(), _stream_handle(stream))
+        else:
+            B.cr_repair_ex(kv.data_ptr(), lay, chunk_offsets, request_chunks,
+                           token_embeds.data_ptr(), self.dims, self.prepared.data_ptr(),
+                           self.prepared_bytes, ws.data_ptr(), ws.numel(), _stream_handle(stream),
+                           options)
+        return kv
+
+    def rotate_keys(self, kv: torch.Tensor, chunk_offsets: Sequence[int],
+                    request_chunks: Optional[Sequence[int]], rope: dict,
+                    position_offset: Optional[Sequence[int]] = None, inverse: bool = False,
+                    layout: Optional[B.cr_kv_layout] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """K <- R_M(p)^(+-1) K in place for every token (cr_rotate_keys)."""
+        n = int(chunk_offsets[-1])
+        lay = layout if layout is not None else self.layout(n)
+        nb = B.cr_rotate_workspace_bytes(lay, n)
+        ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=self.device)
+        B.cr_rotate_keys(kv.data_ptr(), lay, chunk_offsets, request_chunks, rope, position_offset,
+                         inverse, ws.data_ptr(), ws.numel(), _stream_handle(stream))
         return kv

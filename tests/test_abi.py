@@ -175,3 +175,91 @@ def test_workspace_views():
     assert off_s % 256 == 0 and off_h % 256 == 0 and off_s != off_h
     with pytest.raises(B.CrError):
         B.cr_workspace_view(_dims(W0), _layout(W0), 64, "nope")
+
+
+# ------------------------------------------------------------- variants
+def test_option_structs_and_defaults():
+    assert ctypes.sizeof(B.cr_rope) == 24
+    assert ctypes.sizeof(B.cr_options) == 40
+    o = B.cr_options()
+    B.load().cr_default_options(ctypes.byref(o))
+    assert (o.mask, o.reinject, o.residual, o.apply, o.keep_first_chunk) == (0, 1, 1, 0, 0)
+    assert not o.global_rope and not o.position_offset
+
+
+def _call_repair_ex(w, options, layout=None, dims=None):
+    layout = layout or _layout(w)
+    dims = dims or _dims(w)
+    with pytest.raises(B.CrError) as e:
+        B.cr_repair_ex(0x10000, layout, w.chunk_offsets, w.request_chunks, 0x20000, dims,
+                       0x30000, B.cr_prepared_bytes(dims, layout), 0x40000,
+                       B.cr_workspace_bytes(dims, layout, w.n_tokens), None, options)
+    return e.value.name
+
+
+@pytest.mark.parametrize("kw", [dict(mask=4), dict(mask=-1), dict(apply=3), dict(reinject=2),
+                                dict(residual=-1), dict(keep_first_chunk=5),
+                                dict(global_rope=dict(theta=0.0)),
+                                dict(global_rope=dict(theta=1e4, scale=0.0)),
+                                dict(global_rope=dict(inv_freq=[float("nan")] * 16))])
+def test_bad_options(kw):
+    assert _call_repair_ex(W0, B.Options(**kw)) == "CR_ERR_DIMS"
+
+
+def test_bad_global_positions():
+    n_req = len(W0.request_chunks) - 1
+    rope = dict(theta=1e6)
+    assert _call_repair_ex(W0, B.Options(global_rope=rope, position_offset=[-1] * n_req)) == \
+        "CR_ERR_OFFSETS"
+    assert _call_repair_ex(W0, B.Options(global_rope=rope,
+                                         position_offset=[2 ** 31 - 10] * n_req)) == \
+        "CR_ERR_OFFSETS"
+
+
+def test_global_placement_needs_head_dim_at_most_128():
+    w = W.WORKLOADS[1]
+    t = w.target
+    lay = B.layer_major_layout(t.n_layers, t.n_kv_heads, 256, w.n_tokens, B.CR_DTYPE_BF16)
+    assert _call_repair_ex(w, B.Options(global_rope=dict(theta=1e6)), layout=lay) == "CR_ERR_DIMS"
+
+
+def test_options_pointer_is_required():
+    lay = _layout(W0)
+    with pytest.raises(B.CrError) as e:
+        off = np.ascontiguousarray(W0.chunk_offsets, np.int32)
+        st = B.load().cr_repair_ex(0x10000, ctypes.byref(lay),
+                                   off.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                   len(off) - 1, None, 0, 0x20000, ctypes.byref(_dims(W0)),
+                                   0x30000, 1 << 30, 0x40000, 1 << 30, None, None)
+        B._check(st, "cr_repair_ex")
+    assert e.value.name == "CR_ERR_NULL"
+
+
+def _call_rotate(w, rope=None, inverse=0, layout=None, ws_bytes=None, offsets=None,
+                 position_offset=None):
+    layout = layout or _layout(w)
+    offsets = w.chunk_offsets if offsets is None else offsets
+    n = int(offsets[-1])
+    if ws_bytes is None:
+        ws_bytes = B.cr_rotate_workspace_bytes(_layout(w), n)
+    B.cr_rotate_keys(0x10000, layout, offsets, w.request_chunks if offsets is w.chunk_offsets
+                     else None, rope or dict(theta=1e6), position_offset, inverse, 0x40000,
+                     ws_bytes, None)
+
+
+def test_rotate_keys_validation():
+    for kw, name in [(dict(inverse=2), "CR_ERR_DIMS"),
+                     (dict(rope=dict(theta=-1.0)), "CR_ERR_DIMS"),
+                     (dict(ws_bytes=1), "CR_ERR_WORKSPACE"),
+                     (dict(position_offset=[-5] * (len(W0.request_chunks) - 1)), "CR_ERR_OFFSETS")]:
+        with pytest.raises(B.CrError) as e:
+            _call_rotate(W0, **kw)
+        assert e.value.name == name, kw
+    bad = _layout(W0)
+    bad.head_dim = 48
+    with pytest.raises(B.CrError) as e:
+        _call_rotate(W0, layout=bad)
+    assert e.value.name == "CR_ERR_DIMS"
+    # an empty batch returns before touching the device
+    _call_rotate(W0, offsets=np.array([0, 0]), layout=_layout(W0, n=0))
+    assert B.cr_rotate_workspace_bytes(_layout(W0), 100) >= 100 * 16 + 100 * W0.target.head_dim * 4
