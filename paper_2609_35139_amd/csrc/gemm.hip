@@ -5,19 +5,23 @@
 // output tile split in four wave quadrants computed with 32x32 MFMA atoms.
 // K advances in slabs of 128 bytes per row, fetched straight from global
 // memory into an LDS ring with global_load_lds (no register staging); rows
-// are XOR-swizzled in LDS so fragment reads are conflict-free.  The fp32 accumulators are then
-// staged through LDS so that every epilogue reads and writes whole 16-byte
-// row segments (bias, GELU, residual add, RoPE, transposed V, and the
-// strided in-place add into the KV cache).
+// are XOR-swizzled in LDS so fragment reads are conflict-free.  The MFMA
+// takes the weight tile as its first operand, so each lane ends with four
+// consecutive output columns of one output row: the fp32 tile is staged
+// through LDS with 16-byte writes in one pass, after the epilogue has issued
+// its own global loads (bias, residuals, the stale cache), and every
+// epilogue then reads and writes whole 16-byte row segments (bias, GELU,
+// residual adds, RoPE, transposed V, the strided output add into the KV
+// cache with optional global placement of the keys).
 #include "launch.h"
 
 namespace cr {
 
 // Tile geometry: a 2x2 grid of waves, each owning TM x TN MFMA atoms of
-// 32x32 (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32; on
-// gfx950 the 32x32 atoms sustain several times the rate of the 16x16 ones),
-// so the workgroup tile is (64*TM) x (64*TN).  K advances in slabs of one
-// 128-byte row per tile row; STAGES slabs live in the LDS ring.
+// 32x32 (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32), so
+// the workgroup tile is (64*TM) x (64*TN).  K advances in slabs of one
+// 128-byte row per tile row; STAGES slabs live in the LDS ring, which the
+// staged output tile reuses.
 template <typename T, int TM_, int TN_, int STAGES_>
 struct GemmTile {
   static constexpr int TM = TM_, TN = TN_, STAGES = STAGES_;
@@ -30,19 +34,18 @@ struct GemmTile {
   static constexpr int B_ROUNDS = BN * 8 / NT;
   static constexpr int OPS = A_ROUNDS + B_ROUNDS;
   static constexpr int STAGE_BYTES = (BM + BN) * 128;
-  static constexpr int HC = BN / 2;                 // epilogue handles one column half at a time
-  static constexpr int LDC = HC + 4;                // fp32 staging row
+  static constexpr int LDC = BN + 4;                // fp32 staging row (16-byte aligned rows)
   static constexpr size_t LDS_MAIN = (size_t)STAGES * STAGE_BYTES;
   static constexpr size_t LDS_C = (size_t)BM * LDC * sizeof(float);
   static constexpr size_t LDS = LDS_MAIN > LDS_C ? LDS_MAIN : LDS_C;
   static_assert(OPS * (STAGES - 2) <= 63, "vmcnt range");
 };
 
-// Epilogues receive a staged block Cs[ROWS][LDC] (fp32) whose element (r, c)
+// Epilogues see the staged tile Cs[ROWS][LDC] (fp32) whose element (r, c)
 // is output (m0 + r, n0 + c).  Each thread owns one 8-column segment and a
-// strided set of rows, so per-column vectors (bias, sigma) are loaded once
-// and every global load of the segment's rows is issued before any of them
-// is needed.
+// strided set of rows, so per-column vectors (bias, sigma) are loaded once.
+// An epilogue has two phases: prefetch() issues its global loads into a
+// Pre record before the tile is staged, run() consumes the staged tile.
 template <int ROWS, int COLS>
 struct SegMap {
   static constexpr int SEG = COLS / 8;            // segments per row
@@ -60,49 +63,51 @@ __device__ __forceinline__ void load8f(const float* p, float* v) {
 
 template <typename T>
 struct EpiBias {
-  static constexpr bool kFullTile = false;
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
   int64_t ldr2; int gelu;
+  template <int ROWS, int COLS>
+  struct Pre {
+    float b[8];
+    Vec8<T> rv[SegMap<ROWS, COLS>::PASSES], rv2[SegMap<ROWS, COLS>::PASSES];
+  };
+  template <int ROWS, int COLS>
+  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS>;
+    const int gn = n0 + S::col();
+    if (gn >= N) return;
+    load8f(bias + gn, p.b);
+#pragma unroll
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int gm = m0 + S::row(q);
+      if (gm >= M) continue;
+      if (resid) p.rv[q].load(resid + (int64_t)gm * ldr + gn);
+      if (resid2) p.rv2[q].load(resid2 + (int64_t)gm * ldr2 + gn);
+    }
+  }
   template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS>& p, int m0, int n0, int M,
+                      int N) const {
     using S = SegMap<ROWS, COLS>;
     const int c = S::col(), gn = n0 + c;
     if (gn >= N) return;
-    float b[8];
-    load8f(bias + gn, b);
-    Vec8<T> rv[S::PASSES], rv2[S::PASSES];
-    if (resid) {
 #pragma unroll
-      for (int p = 0; p < S::PASSES; ++p) {
-        const int gm = m0 + S::row(p);
-        if (gm < M) rv[p].load(resid + (int64_t)gm * ldr + gn);
-      }
-    }
-    if (resid2) {
-#pragma unroll
-      for (int p = 0; p < S::PASSES; ++p) {
-        const int gm = m0 + S::row(p);
-        if (gm < M) rv2[p].load(resid2 + (int64_t)gm * ldr2 + gn);
-      }
-    }
-#pragma unroll
-    for (int p = 0; p < S::PASSES; ++p) {
-      const int r = S::row(p), gm = m0 + r;
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int r = S::row(q), gm = m0 + r;
       if (gm >= M) continue;
       float v[8];
       load8f(Cs + r * LDC + c, v);
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        v[k] += b[k];
+        v[k] += p.b[k];
         if (gelu) v[k] = gelu_erf(v[k]);
       }
       if (resid) {
-        float rf[8]; rv[p].to_float(rf);
+        float rf[8]; p.rv[q].to_float(rf);
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = rf[k] + v[k];
       }
       if (resid2) {
-        float rf[8]; rv2[p].to_float(rf);
+        float rf[8]; p.rv2[q].to_float(rf);
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = v[k] + rf[k];
       }
@@ -113,57 +118,79 @@ struct EpiBias {
 
 template <typename T>
 struct EpiQKV {
-  static constexpr bool kFullTile = false;
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
+  template <int ROWS, int COLS>
+  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS>::PASSES]; };
+  template <int ROWS, int COLS>
+  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+    if (n0 >= 2 * d_b) return;      // V tiles load their bias per column in run()
+    using S = SegMap<ROWS, COLS>;
+    const int half = d_head / 2;
+    const int c = S::col(), hc = c % d_head;
+    const int pc = hc < half ? c + half : c - half;
+    load8f(bias + n0 + c, p.bx);
+    load8f(bias + n0 + pc, p.by);
+#pragma unroll
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int gm = m0 + S::row(q);
+      p.pp[q] = gm < M ? pos[gm] : 0;
+    }
+  }
   template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS>& p, int m0, int n0, int M,
+                      int N) const {
     if (n0 < 2 * d_b) {
       // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
-      // The block is head-aligned and never straddles Q/K (d_b % COLS == 0).
+      // The tile is head-aligned and never straddles Q/K (d_b % COLS == 0).
       using S = SegMap<ROWS, COLS>;
       T* dst = n0 < d_b ? q : k;
       const int cbase = n0 < d_b ? n0 : n0 - d_b;
       const int half = d_head / 2;
-      const int c = S::col(), gn = n0 + c;
+      const int c = S::col();
       const int hc = c % d_head;
       const bool first = hc < half;
       const int pc = first ? c + half : c - half;
       const int fi = first ? hc : hc - half;
-      float bx[8], by[8];
-      load8f(bias + gn, bx);
-      load8f(bias + n0 + pc, by);
-      int pp[S::PASSES];
+      // the (cos, sin) rows of a group of passes are loaded together
+      constexpr int GRP = S::PASSES >= 4 ? 4 : S::PASSES;
 #pragma unroll
-      for (int p = 0; p < S::PASSES; ++p) {
-        const int gm = m0 + S::row(p);
-        pp[p] = gm < M ? pos[gm] : 0;
+      for (int q0 = 0; q0 < S::PASSES; q0 += GRP) {
+      float4 cs[GRP][4];
+#pragma unroll
+      for (int q = 0; q < GRP; ++q) {
+        const float4* t4 =
+            reinterpret_cast<const float4*>(rope + (int64_t)p.pp[q0 + q] * half + fi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
       }
 #pragma unroll
-      for (int p = 0; p < S::PASSES; ++p) {
-        const int r = S::row(p), gm = m0 + r;
+      for (int q = 0; q < GRP; ++q) {
+        const int qq = q0 + q;
+        const int r = S::row(qq), gm = m0 + r;
         if (gm >= M) continue;
-        const float4* cs4 = reinterpret_cast<const float4*>(rope + (int64_t)pp[p] * half + fi);
         float x[8], y[8], v[8];
         load8f(Cs + r * LDC + c, x);
         load8f(Cs + r * LDC + pc, y);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float4 t = cs4[e];   // (cos, sin) of pairs 2e and 2e+1
-          const float c0 = t.x, s0 = t.y, c1 = t.z, s1 = t.w;
-          const float x0 = x[2 * e] + bx[2 * e], y0 = y[2 * e] + by[2 * e];
-          const float x1 = x[2 * e + 1] + bx[2 * e + 1], y1 = y[2 * e + 1] + by[2 * e + 1];
-          v[2 * e] = first ? x0 * c0 - y0 * s0 : x0 * c0 + y0 * s0;
-          v[2 * e + 1] = first ? x1 * c1 - y1 * s1 : x1 * c1 + y1 * s1;
+          const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
+          const float x0 = x[2 * e] + p.bx[2 * e], y0 = y[2 * e] + p.by[2 * e];
+          const float x1 = x[2 * e + 1] + p.bx[2 * e + 1], y1 = y[2 * e + 1] + p.by[2 * e + 1];
+          v[2 * e] = first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y;
+          v[2 * e + 1] = first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w;
         }
         Vec8<T> o; o.from_float(v); o.store(dst + (int64_t)gm * d_b + cbase + c);
       }
+      }
     } else {
-      // V: write transposed, vt[head][d][token], 8 tokens per store.  Rows
-      // in [M, n_pad) hold values computed from clamped rows: finite padding.
+      // V: written transposed, vt[head][d][token], 8 tokens per 16-byte
+      // store.  Consecutive threads take consecutive columns, so the column
+      // reads of the staged tile are conflict-free.  Rows in [M, n_pad) hold
+      // values computed from clamped rows: finite padding.
       constexpr int RSEG = ROWS / 8;
       for (int idx = threadIdx.x; idx < COLS * RSEG; idx += 256) {
-        const int c = idx / RSEG, r = (idx % RSEG) * 8;
+        const int c = idx % COLS, r = (idx / COLS) * 8;
         const int gn = n0 + c, gm = m0 + r;
         if (gn >= N || gm + 8 > n_pad) continue;
         const int vc = gn - 2 * d_b;
@@ -192,113 +219,151 @@ __device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* 
 
 template <typename T>
 struct EpiExpand {
-  static constexpr bool kFullTile = false;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
+  template <int ROWS, int COLS>
+  struct Pre {
+    float b[8], sg[8];
+    Vec8<T> x[SegMap<ROWS, COLS>::PASSES];
+    int kp[SegMap<ROWS, COLS>::PASSES];
+  };
+  // 8 | d_h keeps a segment in one head
+  __device__ bool selected(int gn, T** base) const {
+    bool is_k;
+    *base = kv_coord(kv, ks, gn, &is_k);
+    return mode & (is_k ? EXPAND_K : EXPAND_V);
+  }
+  template <int ROWS, int COLS>
+  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS>;
+    const int gn = n0 + S::col();
+    T* base;
+    if (gn >= N || !selected(gn, &base)) return;   // unselected component: left stale
+    load8f(bias + gn, p.b);
+    load8f(sigma + gn, p.sg);
+#pragma unroll
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int gm = m0 + S::row(q);
+      p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
+      if (gm < M && (mode & EXPAND_RESIDUAL)) p.x[q].load(base + (int64_t)gm * ks.token);
+    }
+  }
   template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
+  __device__ void run(const float* Cs, Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS>;
     const int c = S::col(), gn = n0 + c;
-    if (gn >= N) return;
-    // 8 | d_h keeps a segment in one head
-    bool is_k;
-    T* base = kv_coord(kv, ks, gn, &is_k);
-    if (!(mode & (is_k ? EXPAND_K : EXPAND_V))) return;   // component left stale
+    T* base;
+    if (gn >= N || !selected(gn, &base)) return;
     const bool res = mode & EXPAND_RESIDUAL;
-    float b[8], sg[8];
-    load8f(bias + gn, b);
-    load8f(sigma + gn, sg);
-    Vec8<T> x[S::PASSES];
-    int kp[S::PASSES];
 #pragma unroll
-    for (int p = 0; p < S::PASSES; ++p) {
-      const int gm = m0 + S::row(p);
-      kp[p] = (gm < M && keep) ? keep[gm] : 0;
-      if (gm < M && res) x[p].load(base + (int64_t)gm * ks.token);
-    }
-#pragma unroll
-    for (int p = 0; p < S::PASSES; ++p) {
-      const int r = S::row(p), gm = m0 + r;
-      if (gm >= M || kp[p]) continue;
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int r = S::row(q), gm = m0 + r;
+      if (gm >= M || p.kp[q]) continue;
       float a[8], f[8];
       load8f(Cs + r * LDC + c, a);
-      if (res) x[p].to_float(f);
+      if (res) p.x[q].to_float(f);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + sg[e] * (a[e] + b[e]);
-      x[p].from_float(f);
-      x[p].store(base + (int64_t)gm * ks.token);
+      for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + p.sg[e] * (a[e] + p.b[e]);
+      p.x[q].from_float(f);
+      p.x[q].store(base + (int64_t)gm * ks.token);
     }
   }
 };
 
 // Output add followed by the target model's rotation of every key head
-// (global placement), on a fully staged tile: a thread owns 8 rotate-half
-// pairs (columns c .. c+7 and c+half .. c+half+7 of one head) of a set of
-// rows, so both members of every pair are rotated in registers.  Requires
-// head_dim <= 128 (a head never straddles two 128-column tiles).
+// (global placement): a thread owns 8 rotate-half pairs (columns c .. c+7 and
+// c+half .. c+half+7 of one head) of a set of rows, so both members of every
+// pair are rotated in registers.  Requires head_dim <= 128 (a head never
+// straddles two 128-column tiles).
 template <typename T>
 struct EpiExpandRope {
-  static constexpr bool kFullTile = true;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   const float2* rope;   // [M][head_dim/2] scaled (cos, sin)
-  template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, int m0, int n0, int M, int N) const {
-    constexpr int PAIRS = COLS / 16;               // 8-pair groups per tile row
-    constexpr int RSTEP = 256 / PAIRS, PASSES = ROWS / RSTEP;
+  template <int COLS> struct Map {
+    static constexpr int PAIRS = COLS / 16;        // 8-pair groups per tile row
+    static constexpr int RSTEP = 256 / PAIRS;
+  };
+  template <int ROWS, int COLS>
+  struct Pre {
+    static constexpr int P = ROWS / Map<COLS>::RSTEP;
+    float b1[8], b2[8], s1[8], s2[8];
+    Vec8<T> x1[P], x2[P];
+    int kp[P];
+  };
+  struct Cols { int c1, c2, i0; bool is_k, on; T* b1; };
+  template <int COLS>
+  __device__ bool cols(int n0, int N, Cols& k) const {
     const int dh = ks.head_dim, half = dh / 2, sph = half / 8;
-    const int p = threadIdx.x % PAIRS;
-    const int c1 = (p / sph) * dh + (p % sph) * 8, c2 = c1 + half;
-    const int g1 = n0 + c1, g2 = n0 + c2;
-    if (g2 >= N) return;
-    bool is_k;
-    T* b1 = kv_coord(kv, ks, g1, &is_k);
-    T* b2 = b1 + half;
-    const int i0 = g1 % dh;
-    const bool on = mode & (is_k ? EXPAND_K : EXPAND_V);
-    if (!on && !is_k) return;                      // stale V: nothing to write
-    const bool res = mode & EXPAND_RESIDUAL;
-    float bb1[8], bb2[8], s1[8], s2[8];
-    load8f(bias + g1, bb1); load8f(bias + g2, bb2);
-    load8f(sigma + g1, s1); load8f(sigma + g2, s2);
-    Vec8<T> x1[PASSES], x2[PASSES];
-    int kp[PASSES];
-    float4 cs[PASSES][4];
+    const int p = threadIdx.x % Map<COLS>::PAIRS;
+    k.c1 = (p / sph) * dh + (p % sph) * 8;
+    k.c2 = k.c1 + half;
+    if (n0 + k.c2 >= N) return false;
+    k.b1 = kv_coord(kv, ks, n0 + k.c1, &k.is_k);
+    k.i0 = (n0 + k.c1) % dh;
+    k.on = mode & (k.is_k ? EXPAND_K : EXPAND_V);
+    return k.on || k.is_k;                         // stale V: nothing to write
+  }
+  template <int ROWS, int COLS>
+  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+    Cols k;
+    if (!cols<COLS>(n0, N, k)) return;
+    const int half = ks.head_dim / 2;
+    load8f(bias + n0 + k.c1, p.b1); load8f(bias + n0 + k.c2, p.b2);
+    load8f(sigma + n0 + k.c1, p.s1); load8f(sigma + n0 + k.c2, p.s2);
 #pragma unroll
-    for (int q = 0; q < PASSES; ++q) {
-      const int gm = m0 + threadIdx.x / PAIRS + q * RSTEP;
-      kp[q] = (gm < M && keep) ? keep[gm] : 0;
+    for (int q = 0; q < Pre<ROWS, COLS>::P; ++q) {
+      const int gm = m0 + threadIdx.x / Map<COLS>::PAIRS + q * Map<COLS>::RSTEP;
+      p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
       if (gm < M) {
-        x1[q].load(b1 + (int64_t)gm * ks.token);
-        x2[q].load(b2 + (int64_t)gm * ks.token);
-        if (is_k) {
-          const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)gm * half + i0);
+        p.x1[q].load(k.b1 + (int64_t)gm * ks.token);
+        p.x2[q].load(k.b1 + half + (int64_t)gm * ks.token);
+      }
+    }
+  }
+  template <int ROWS, int COLS, int LDC>
+  __device__ void run(const float* Cs, Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+    Cols k;
+    if (!cols<COLS>(n0, N, k)) return;
+    const int half = ks.head_dim / 2;
+    constexpr int P = Pre<ROWS, COLS>::P;
+    const bool res = mode & EXPAND_RESIDUAL;
+    constexpr int GRP = P >= 2 ? 2 : P;             // passes whose (cos, sin) load together
 #pragma unroll
-          for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
-        }
+    for (int q0 = 0; q0 < P; q0 += GRP) {
+    float4 cs[GRP][4];
+    if (k.is_k) {
+#pragma unroll
+      for (int u = 0; u < GRP; ++u) {
+        const int gm =
+            min(m0 + (int)threadIdx.x / Map<COLS>::PAIRS + (q0 + u) * Map<COLS>::RSTEP, M - 1);
+        const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)gm * half + k.i0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[u][e] = t4[e];
       }
     }
 #pragma unroll
-    for (int q = 0; q < PASSES; ++q) {
-      const int r = threadIdx.x / PAIRS + q * RSTEP, gm = m0 + r;
+    for (int u = 0; u < GRP; ++u) {
+      const int q = q0 + u;
+      const int r = threadIdx.x / Map<COLS>::PAIRS + q * Map<COLS>::RSTEP, gm = m0 + r;
       if (gm >= M) continue;
       float y1[8], y2[8];
-      x1[q].to_float(y1);
-      x2[q].to_float(y2);
-      if (on && !kp[q]) {
+      p.x1[q].to_float(y1);
+      p.x2[q].to_float(y2);
+      if (k.on && !p.kp[q]) {
         float a1[8], a2[8];
-        load8f(Cs + r * LDC + c1, a1);
-        load8f(Cs + r * LDC + c2, a2);
+        load8f(Cs + r * LDC + k.c1, a1);
+        load8f(Cs + r * LDC + k.c2, a2);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          y1[e] = (res ? y1[e] : 0.f) + s1[e] * (a1[e] + bb1[e]);
-          y2[e] = (res ? y2[e] : 0.f) + s2[e] * (a2[e] + bb2[e]);
+          y1[e] = (res ? y1[e] : 0.f) + p.s1[e] * (a1[e] + p.b1[e]);
+          y2[e] = (res ? y2[e] : 0.f) + p.s2[e] * (a2[e] + p.b2[e]);
         }
-      } else if (!is_k) {
+      } else if (!k.is_k) {
         continue;
       }
-      if (is_k) {
+      if (k.is_k) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
+          const float4 t = cs[u][e];   // (cos, sin) of pairs 2e and 2e+1
           const float u0 = y1[2 * e], v0 = y2[2 * e], u1 = y1[2 * e + 1], v1 = y2[2 * e + 1];
           y1[2 * e] = t.x * u0 - t.y * v0;
           y2[2 * e] = t.x * v0 + t.y * u0;
@@ -306,10 +371,11 @@ struct EpiExpandRope {
           y2[2 * e + 1] = t.z * v1 + t.w * u1;
         }
       }
-      x1[q].from_float(y1);
-      x2[q].from_float(y2);
-      x1[q].store(b1 + (int64_t)gm * ks.token);
-      x2[q].store(b2 + (int64_t)gm * ks.token);
+      p.x1[q].from_float(y1);
+      p.x2[q].from_float(y2);
+      p.x1[q].store(k.b1 + (int64_t)gm * ks.token);
+      p.x2[q].store(k.b1 + half + (int64_t)gm * ks.token);
+    }
     }
   }
 };
@@ -330,9 +396,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
                                                       int M, int N, int K, Epi epi) {
   using MM = Mma32<T>;
   using frag = typename MM::frag;
-  constexpr int LDCF = G::BN + 4;                    // full-tile staging row
-  constexpr size_t LDS_FULL = Epi::kFullTile ? (size_t)G::BM * LDCF * sizeof(float) : 0;
-  __shared__ __align__(1024) char smem[G::LDS > LDS_FULL ? G::LDS : LDS_FULL];
+  __shared__ __align__(1024) char smem[G::LDS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.y * G::BM, n0 = blockIdx.x * G::BN;
@@ -399,46 +463,31 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
 #pragma unroll
       for (int i = 0; i < G::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < G::TN; ++j) acc[i][j] = MM::mma(af[i], bfr[j], acc[i][j]);
+        for (int j = 0; j < G::TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
     }
   }
 
-  // Epilogue in two column halves: the waves owning half p stage their
-  // accumulators (32x32 layout: lane holds column lane%32, register
-  // v holds row (v/4)*8 + (lane/32)*4 + v%4), then all threads run the
-  // epilogue on that half.
+  // Epilogue.  With the weight tile as the MFMA's first operand, lane l of
+  // atom (i, j) holds output row wm + i*32 + (l & 31) and, in registers
+  // 4g .. 4g+3, the consecutive columns wn + j*32 + 8g + 4*(l >> 5) + [0, 4).
+  // The epilogue's global loads go out first; the tile is then staged whole
+  // with 16-byte LDS writes over the ring.
+  typename Epi::template Pre<G::BM, G::BN> pre;
+  epi.template prefetch<G::BM, G::BN>(pre, m0, n0, M, N);
+  __syncthreads();  // ring no longer read
   float* Cs = reinterpret_cast<float*>(smem);
-  if constexpr (Epi::kFullTile) {
-    // epilogues that pair columns across the two halves see the whole tile
-    __syncthreads();  // ring no longer read
 #pragma unroll
-    for (int i = 0; i < G::TM; ++i)
+  for (int i = 0; i < G::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < G::TN; ++j)
+    for (int j = 0; j < G::TN; ++j)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          Cs[(wm + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * LDCF + wn + j * 32 + fr] =
-              acc[i][j][v];
-    __syncthreads();
-    epi.template run<G::BM, G::BN, LDCF>(Cs, m0, n0, M, N);
-    return;
-  }
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    __syncthreads();  // ring (or the previous half) no longer read
-    if ((wave & 1) == p) {
-#pragma unroll
-      for (int i = 0; i < G::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < G::TN; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            Cs[(wm + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3)) * G::LDC + j * 32 + fr] =
-                acc[i][j][v];
-    }
-    __syncthreads();
-    epi.template run<G::BM, G::HC, G::LDC>(Cs, m0, n0 + p * G::HC, M, N);
-  }
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(Cs + (wm + i * 32 + fr) * G::LDC + wn + j * 32 + g * 8 +
+                                   (lane >> 5) * 4) =
+            make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                        acc[i][j][4 * g + 3]);
+  __syncthreads();
+  epi.template run<G::BM, G::BN, G::LDC>(Cs, pre, m0, n0, M, N);
 }
 
 template <typename T, typename G, typename Epi>
