@@ -265,7 +265,7 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.h = a.take(N * db * T);
   w.a = a.take(N * db * T);
   w.q = a.take(N * db * T);
-  w.k = a.take(N * db * T);
+  w.k = a.take(w.n_pad * db * T);     // key rows padded like V^T
   w.vt = a.take(db * w.n_pad * T);
   w.o = a.take(N * db * T);
   w.f = a.take(N * r * db * T);

@@ -23,12 +23,13 @@
 // 2^8 (in exp2 units), which keeps probabilities <= 256 and skips almost
 // every rescale of the output accumulators.
 #include <climits>
+#include <type_traits>
 
 #include "launch.h"
 
 namespace cr {
 
-template <typename T, int D, int STAGES_ = 3>
+template <typename T, int D, int STAGES_ = 4>
 struct AttnCfg {
   static constexpr int BQ = 128, BKV = 64, STAGES = STAGES_;
   static constexpr int GROUPS = 2, NT = 256 * GROUPS;  // two 4-wave groups
@@ -58,7 +59,12 @@ __device__ __forceinline__ int score_key(int g, int i) { return (i >> 3) * 16 + 
 // 0's at the end.  This halves the critical path of the long query tiles of
 // late chunks and keeps two waves per SIMD so that one wave's softmax
 // overlaps the other's MFMAs.
-template <typename T, int D, int STAGES = 3>
+//
+// Q arrives pre-scaled by log2(e)/sqrt(d_head) (QKV epilogue), so scores are
+// in exp2 units.  K and V^T are padded with finite rows up to n_pad, so tile
+// loads need no clamping.  The tile loop is unrolled over the STAGES ring
+// slots: every LDS address is a per-lane base plus a compile-time offset.
+template <typename T, int D, int STAGES = 4>
 __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
                                                         const T* __restrict__ Kg,
                                                         const T* __restrict__ Vt,
@@ -66,7 +72,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
                                                         int n_heads, int64_t n_pad,
                                                         const int* __restrict__ lo_arr,
                                                         const int* __restrict__ hi_arr,
-                                                        float scale_log2, int n_qtiles) {
+                                                        int n_qtiles) {
   using C = AttnCfg<T, D, STAGES>;
   using MM = Mma32<T>;
   using frag = typename MM::frag;
@@ -75,11 +81,12 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   constexpr int KPL = MM::KPL, KSTEP = MM::KSTEP;
   constexpr int QF = D / KSTEP;          // Q fragments per lane
   constexpr int DT = D / 32;             // 32-row tiles of O^T
+  constexpr int PS = 32 / KSTEP;         // P fragments per 32-key sub-tile
   __shared__ __align__(1024) char lds[C::LDS];
   __shared__ int red[2][4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int grp = wave >> 2, gw = wave & 3, gtid = tid & 255;
+  const int grp = wave >> 2, gw = wave & 3;
   const int g = lane >> 5, ql = lane & 31;
   const int head = blockIdx.x % n_heads;
   const int qt = n_qtiles - 1 - blockIdx.x / n_heads;   // latest (longest) tiles first
@@ -114,17 +121,15 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     else qf[s] = frag{};
   }
 
-  // DMA sources (per lane): K rows are keys (clamped to N-1 past the end:
-  // such keys are always masked), V^T rows are d.
+  // DMA sources (per lane) of the workgroup's first key tile: K rows are
+  // keys, V^T rows are d.  Both are padded to n_pad >= roundup(N, 64) keys.
   const char* ksrc[C::K_ROUNDS];
   const char* vsrc[C::V_ROUNDS];
-  int krow0[C::K_ROUNDS];
 #pragma unroll
   for (int r = 0; r < C::K_ROUNDS; ++r) {
     const int row = (r * 4 + gw) * SK::RPW + lane / SK::CPR;
-    krow0[r] = row;
     const int chunk = SK::slot(row, lane % SK::CPR);
-    ksrc[r] = reinterpret_cast<const char*>(Kg + head * D) + chunk * 16;
+    ksrc[r] = reinterpret_cast<const char*>(Kg + (int64_t)(kb + row) * d_b + head * D) + chunk * 16;
   }
 #pragma unroll
   for (int r = 0; r < C::V_ROUNDS; ++r) {
@@ -132,63 +137,75 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     const int chunk = SV::slot(row, lane % SV::CPR);
     vsrc[r] = reinterpret_cast<const char*>(Vt + ((int64_t)head * D + row) * n_pad + kb) + chunk * 16;
   }
-  const int64_t krow_bytes = (int64_t)d_b * sizeof(T);
+  const int64_t ktile_bytes = (int64_t)C::BKV * d_b * sizeof(T);
+
+  // per-lane LDS read addresses inside slot 0 of the ring: K fragment kk of
+  // sub-tile 0 (sub-tile 1 is 32 rows further; the swizzle is periodic in 32
+  // rows), and the V^T fragment of sub-tile rt, P fragment s2 (dt adds 32 rows)
+  const int krow = swap_bits23(ql);
+  const char* kp[QF];
+#pragma unroll
+  for (int kk = 0; kk < QF; ++kk) {
+    const int k = kk * KSTEP + g * KPL;
+    kp[kk] = ring + SK::offset(krow, k / C::VEC) + (k % C::VEC) * (int)sizeof(T);
+  }
+  const char* vp[2][PS];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int s2 = 0; s2 < PS; ++s2) {
+      const int kofs = rt * 32 + score_key(g, s2 * KPL);
+      vp[rt][s2] = ring + C::K_BYTES + SV::offset(ql, kofs / C::VEC) + (kofs % C::VEC) * (int)sizeof(T);
+    }
 
   f32x16 oacc[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) oacc[d] = f32x16{};
   float m_ref = -INFINITY, lsum = 0.f;
-  const int krow = swap_bits23(ql);
 
-  // group-local tile i is workgroup tile 2i + grp
-#define CR_ATTN_ISSUE(I, STAGE)                                                            \
-  do {                                                                                     \
-    char* base_ = ring + (STAGE) * C::STAGE_BYTES;                                         \
-    const int tile_ = 2 * (I) + grp;                                                       \
-    const int k0_ = kb + tile_ * C::BKV;                                                   \
-    _Pragma("unroll") for (int r = 0; r < C::K_ROUNDS; ++r) {                              \
-      const int key_ = min(k0_ + krow0[r], N - 1);                                         \
-      dma16(ksrc[r] + key_ * krow_bytes, base_ + (r * 4 + gw) * 1024);                     \
-    }                                                                                      \
-    _Pragma("unroll") for (int r = 0; r < C::V_ROUNDS; ++r)                                \
-      dma16(vsrc[r] + (int64_t)tile_ * C::BKV * sizeof(T),                                 \
-            base_ + C::K_BYTES + (r * 4 + gw) * 1024);                                     \
-  } while (0)
-
+  // group-local tile i (workgroup tile 2i + grp) into ring slot SLOT
+  auto issue = [&](int i, int slot_bytes) {
+    char* base = ring + slot_bytes;
+    const int64_t tile = 2 * i + grp;
 #pragma unroll
-  for (int st = 0; st < C::STAGES - 1; ++st)
-    if (st < mine) CR_ATTN_ISSUE(st, st);
+    for (int r = 0; r < C::K_ROUNDS; ++r)
+      dma16(ksrc[r] + tile * ktile_bytes, base + (r * 4 + gw) * 1024);
+#pragma unroll
+    for (int r = 0; r < C::V_ROUNDS; ++r)
+      dma16(vsrc[r] + tile * C::BKV * (int64_t)sizeof(T), base + C::K_BYTES + (r * 4 + gw) * 1024);
+  };
 
-  for (int it = 0; it < iters; ++it) {
-    // this group's slab `it` has landed once min(STAGES-2, mine-1-it) later ones remain
+  // one key tile held in ring slot J (compile time)
+  auto step = [&](auto slot, int it) {
+    constexpr int J = decltype(slot)::value;
+    if (it >= iters) return;
+    // this group's tile `it` has landed once min(STAGES-2, mine-1-it) later ones remain
     const int ahead = min(C::STAGES - 2, mine - 1 - it);
     if (C::STAGES >= 4 && ahead >= 2) wait_vmcnt<2 * C::OPS>();
     else if (C::STAGES >= 3 && ahead >= 1) wait_vmcnt<C::OPS>();
     else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    if (it + C::STAGES - 1 < mine) CR_ATTN_ISSUE(it + C::STAGES - 1, (it + C::STAGES - 1) % C::STAGES);
-    if (it >= mine) continue;   // group 1 without a last tile: only keeps the barrier count
+    __builtin_amdgcn_s_barrier();   // the slot refilled below is no longer read by anyone
+    if (it + C::STAGES - 1 < mine)
+      issue(it + C::STAGES - 1, ((J + C::STAGES - 1) % C::STAGES) * C::STAGE_BYTES);
+    if (it >= mine) return;         // group 1 without a last tile: only keeps the barrier count
+    constexpr int SO = J * C::STAGE_BYTES;
 
-    const char* ks_ = ring + (it % C::STAGES) * C::STAGE_BYTES;
-    const char* vs_ = ks_ + C::K_BYTES;
-    const int k0 = kb + (2 * it + grp) * C::BKV;
-
-    // S^T for two 32-key sub-tiles
+    // S^T = K Q^T for two 32-key sub-tiles; all fragment reads first
+    frag kf[2][QF];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int kk = 0; kk < QF; ++kk)
+        kf[rt][kk] = *reinterpret_cast<const frag*>(kp[kk] + (SO + rt * 32 * C::RBK));
     f32x16 s[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       s[rt] = f32x16{};
-      const int row = rt * 32 + krow;
 #pragma unroll
-      for (int ks = 0; ks < QF; ++ks) {
-        const int k = ks * KSTEP + g * KPL;
-        const frag a = *reinterpret_cast<const frag*>(ks_ + SK::offset(row, k / C::VEC) +
-                                                      (k % C::VEC) * (int)sizeof(T));
-        s[rt] = MM::mma(a, qf[ks], s[rt]);
-      }
+      for (int kk = 0; kk < QF; ++kk) s[rt] = MM::mma(kf[rt][kk], qf[kk], s[rt]);
     }
-    const bool need_mask = !(k0 >= wmax_lo && k0 + C::BKV <= wmin_hi);
-    if (need_mask) {
+    const int k0 = kb + (2 * it + grp) * C::BKV;
+    if (!(k0 >= wmax_lo && k0 + C::BKV <= wmin_hi)) {
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
@@ -202,7 +219,9 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rt][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE)) * scale_log2;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+    // the reference max only moves when a row max exceeds it by 2^8 in
+    // exp2 units: probabilities stay <= 256 and rescales are rare
     if (__any(mx > m_ref + 8.0f)) {
       const float m_new = fmaxf(m_ref, mx);
       const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_ref - m_new);
@@ -214,36 +233,45 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
         for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
     }
     const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
-    float psum = 0.f;
+    // probabilities packed straight into the B operand of P V; the row sum
+    // is taken over the packed values the product uses
+    frag pb[2][PS];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rt][i], scale_log2, -m_use));
-        s[rt][i] = p;
-        psum += p;
-      }
-    lsum += psum;
-
-    // O^T += V^T P^T
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int s2 = 0; s2 < 32 / KSTEP; ++s2) {
+      for (int s2 = 0; s2 < PS; ++s2) {
         float pv[KPL];
 #pragma unroll
-        for (int e = 0; e < KPL; ++e) pv[e] = s[rt][s2 * KPL + e];
-        const frag b = pack_frag(pv, (frag*)nullptr);
-        const int kofs = rt * 32 + score_key(g, s2 * KPL);
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const frag a = *reinterpret_cast<const frag*>(
-              vs_ + SV::offset(d * 32 + ql, kofs / C::VEC) + (kofs % C::VEC) * (int)sizeof(T));
-          oacc[d] = MM::mma(a, b, oacc[d]);
-        }
+        for (int e = 0; e < KPL; ++e) pv[e] = __builtin_amdgcn_exp2f(s[rt][s2 * KPL + e] - m_use);
+        pb[rt][s2] = pack_frag(pv, (frag*)nullptr);
+        lsum = frag_sum(pb[rt][s2], lsum);
       }
+    // O^T += V^T P^T; all fragment reads first
+    frag vf[2][PS][DT];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int s2 = 0; s2 < PS; ++s2)
+#pragma unroll
+        for (int d = 0; d < DT; ++d)
+          vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int s2 = 0; s2 < PS; ++s2)
+#pragma unroll
+        for (int d = 0; d < DT; ++d) oacc[d] = MM::mma(vf[rt][s2][d], pb[rt][s2], oacc[d]);
+  };
+
+#pragma unroll
+  for (int st = 0; st < C::STAGES - 1; ++st)
+    if (st < mine) issue(st, st * C::STAGE_BYTES);
+  for (int it0 = 0; it0 < iters; it0 += C::STAGES) {
+    step(std::integral_constant<int, 0>{}, it0);
+    step(std::integral_constant<int, 1>{}, it0 + 1);
+    if constexpr (C::STAGES > 2) step(std::integral_constant<int, 2 % C::STAGES>{}, it0 + 2);
+    if constexpr (C::STAGES > 3) step(std::integral_constant<int, 3 % C::STAGES>{}, it0 + 3);
   }
-#undef CR_ATTN_ISSUE
 
   // merge group 1 into group 0: per query q' = gw*32 + ql, lane half g holds
   // l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4 of O^T
@@ -291,16 +319,17 @@ template <typename T>
 hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, int n_heads,
                      int d_head, int64_t n_pad, const int* lo, const int* hi, hipStream_t s) {
   if (N <= 0) return hipSuccess;
+  if (n_pad < ((N + 63) / 64) * 64) return hipErrorInvalidValue;
   const int n_qtiles = (N + 127) / 128;
-  const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)d_head));
   dim3 grid(n_qtiles * n_heads);
-  constexpr int kStages = sizeof(T) == 2 ? 3 : 2;   // two rings must fit in 160 KB of LDS
+  // two rings (one per wave group) must fit in 160 KB of LDS
+  constexpr int kStages = sizeof(T) == 2 ? 4 : 2;
   if (d_head == 64) {
     CR_LAUNCH((attention_kernel<T, 64, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
-                       n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
+              n_heads, n_pad, lo, hi, n_qtiles);
   } else if (d_head == 32) {
     CR_LAUNCH((attention_kernel<T, 32, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
-                       n_heads, n_pad, lo, hi, scale_log2, n_qtiles);
+              n_heads, n_pad, lo, hi, n_qtiles);
   } else {
     return hipErrorInvalidValue;
   }

@@ -118,6 +118,20 @@ __device__ __forceinline__ bf16x8 pack_frag(const float* f, bf16x8*) {
 }
 __device__ __forceinline__ float pack_frag(const float* f, float*) { return f[0]; }
 
+// Sum of the elements of an operand fragment, accumulated in fp32
+// (bf16 pairs through v_dot2_f32_bf16 against (1, 1)).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float frag_sum(bf16x8 v, float acc) {
+  const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 pr = {v[2 * i], v[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+  }
+  return acc;
+}
+__device__ __forceinline__ float frag_sum(float v, float acc) { return acc + v; }
+
 // ------------------------------------------------- direct global -> LDS
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;

@@ -143,8 +143,14 @@ struct EpiQKV {
     if (n0 < 2 * d_b) {
       // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
       // The tile is head-aligned and never straddles Q/K (d_b % COLS == 0).
+      // Q leaves scaled by log2(e)/sqrt(d_head) (the attention works in exp2
+      // units); K rows in [M, n_pad) get finite values from clamped rows
+      // (padding read by the attention's last key tile).
       using S = SegMap<ROWS, COLS>;
-      T* dst = n0 < d_b ? q : k;
+      const bool is_q = n0 < d_b;
+      T* dst = is_q ? q : k;
+      const int rows_out = is_q ? M : (int)n_pad;
+      const float osc = is_q ? 1.4426950408889634f / __builtin_sqrtf((float)d_head) : 1.0f;
       const int cbase = n0 < d_b ? n0 : n0 - d_b;
       const int half = d_head / 2;
       const int c = S::col();
@@ -168,7 +174,7 @@ struct EpiQKV {
       for (int q = 0; q < GRP; ++q) {
         const int qq = q0 + q;
         const int r = S::row(qq), gm = m0 + r;
-        if (gm >= M) continue;
+        if (gm >= rows_out) continue;
         float x[8], y[8], v[8];
         load8f(Cs + r * LDC + c, x);
         load8f(Cs + r * LDC + pc, y);
@@ -177,8 +183,8 @@ struct EpiQKV {
           const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
           const float x0 = x[2 * e] + p.bx[2 * e], y0 = y[2 * e] + p.by[2 * e];
           const float x1 = x[2 * e + 1] + p.bx[2 * e + 1], y1 = y[2 * e + 1] + p.by[2 * e + 1];
-          v[2 * e] = first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y;
-          v[2 * e + 1] = first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w;
+          v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
+          v[2 * e + 1] = (first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w) * osc;
         }
         Vec8<T> o; o.from_float(v); o.store(dst + (int64_t)gm * d_b + cbase + c);
       }

@@ -40,8 +40,9 @@ hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, in
                      bool gelu, hipStream_t s, const T* resid2 = nullptr, int64_t ldr2 = 0);
 
 // QKV projection with the repair backbone's RoPE on Q and K (rotate-half
-// pairs, table rope[pos][d_head/2] of (cos, sin)); V is written transposed,
-// vt[head][d][n_pad].
+// pairs, table rope[pos][d_head/2] of (cos, sin)); Q is written scaled by
+// log2(e)/sqrt(d_head); K rows and V^T columns are written up to n_pad
+// (finite padding); V is written transposed, vt[head][d][n_pad].
 template <typename T>
 hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
                     T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
@@ -61,7 +62,8 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
                        KvStrides ks, const float* bias, const float* sigma, int mode,
                        const int* keep, const float2* key_rope, hipStream_t s);
 
-// ---- block-causal flash attention (per-row key interval [lo, hi)).
+// ---- flash attention over per-row key intervals [lo, hi); q pre-scaled by
+// log2(e)/sqrt(d_head); k and vt padded to n_pad >= roundup(N, 64) keys.
 template <typename T>
 hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, int n_heads,
                      int d_head, int64_t n_pad, const int* lo, const int* hi, hipStream_t s);
