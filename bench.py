@@ -290,6 +290,33 @@ def main():
         torch.cuda.synchronize()
         vms = a.elapsed_time(b) / vsteps
         variants[name] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
+    # paged cache: the same batch in a pool of 16-token blocks under a
+    # shuffled block table, repaired in place through the table
+    bs = 16
+    nbt = -(-w.n_tokens // bs)
+    table = np.random.default_rng(0).permutation(nbt).astype(np.int32)
+    pool = torch.empty((t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim), dtype=kv.dtype,
+                       device="cuda")
+    flat = kv.view(t.n_layers, 2, w.n_tokens, t.n_kv_heads, t.head_dim)
+    pad = nbt * bs - w.n_tokens
+    src = torch.nn.functional.pad(flat, (0, 0, 0, 0, 0, pad)) if pad else flat
+    pool[:, :, torch.from_numpy(table).long().cuda()] = src.reshape(
+        t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim)
+    plan, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, nbt, bs,
+                              B.CR_DTYPE_BF16 if w.dtype == "bf16" else B.CR_DTYPE_F32)
+    popt = B.Options(pages=dict(block_size=bs, n_blocks=nbt, stride_block=sB,
+                                block_table=table))
+    for _ in range(2):
+        rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(vsteps):
+        rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
+    b.record(stream)
+    torch.cuda.synchronize()
+    vms = a.elapsed_time(b) / vsteps
+    variants["paged_16_token_blocks"] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
+    del pool
     print("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in
                                             variants.items()), file=sys.stderr, flush=True)
 

@@ -264,7 +264,34 @@ typedef struct {
  *                    length of a cached preamble); p_t = position_offset[r] +
  *                    position of t within its request.  Each p_t must be
  *                    non-negative and below 2^31 - 1.
+ *  pages:            NULL, or a paged cache layout (cr_kv_pages).
  */
+/*
+ * Paged cache (the block-table layout of paged serving caches; the paper's
+ * baselines inject repaired prefixes into a paged cache of 16-token blocks,
+ * appendix "Cached-prefix execution", and time that write separately, Table
+ * tab:repair-latency-components, "KV write").  With pages, the repair reads
+ * and writes the blocks in place and no separate write is needed.
+ * Token t of the batch lives in block block_table[t / block_size], row
+ * t % block_size, so element (l, kv, t, h, i) is at
+ *   base + l*stride_layer + kv*stride_kv + block_table[t / block_size]*stride_block
+ *        + (t % block_size)*stride_token + h*stride_head + i
+ * (stride_* other than stride_block from cr_kv_layout).
+ *  block_size:   tokens per block, a power of two, 1..1024.
+ *  n_blocks:     blocks the cache holds (block ids lie in [0, n_blocks)).
+ *  stride_block: elements between consecutive blocks (a multiple of 8).
+ *  block_table:  host, ceil(N / block_size) distinct block ids.
+ * The strides must be injective over (layer, kv, block, row, head, dim) for
+ * n_blocks blocks; otherwise CR_ERR_LAYOUT.  A bad table (id out of range or
+ * repeated) gives CR_ERR_LAYOUT before anything is enqueued.
+ */
+typedef struct {
+    int32_t block_size;
+    int32_t n_blocks;
+    int64_t stride_block;
+    const int32_t* block_table;
+} cr_kv_pages;
+
 typedef struct {
     int32_t mask;
     int32_t reinject;
@@ -273,6 +300,7 @@ typedef struct {
     int32_t keep_first_chunk;
     const cr_rope* global_rope;
     const int32_t* position_offset;
+    const cr_kv_pages* pages;    /* NULL = the strided layout of cr_kv_layout */
 } cr_options;
 
 /* Fills opt with the method's options. */
@@ -301,8 +329,9 @@ CR_API cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout,
  * chunk caches into canonical coordinates (paper Section 4.1, "Chunk-cache
  * preparation"); inverse = 0 places canonical keys at global positions.
  * kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests: as
- * cr_repair.  workspace: device, at least cr_rotate_workspace_bytes bytes,
- * 256-byte aligned.  Requires head_dim <= 256.  Errors as cr_repair_ex.
+ * cr_repair; pages: NULL or a paged layout (cr_kv_pages).  workspace: device,
+ * at least cr_rotate_workspace_bytes bytes, 256-byte aligned.  Requires
+ * head_dim <= 256.  Errors as cr_repair_ex.
  */
 CR_API cr_status cr_rotate_workspace_bytes(const cr_kv_layout* layout, int64_t n_tokens,
                                     uint64_t* bytes);
@@ -310,8 +339,8 @@ CR_API cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout,
                          const int32_t* chunk_offsets, int32_t n_chunks,
                          const int32_t* request_chunks, int32_t n_requests,
                          const cr_rope* rope, const int32_t* position_offset,
-                         int32_t inverse, void* workspace, uint64_t workspace_bytes,
-                         void* stream);
+                         int32_t inverse, const cr_kv_pages* pages,
+                         void* workspace, uint64_t workspace_bytes, void* stream);
 
 /*
  * Debug view into the workspace after a cr_repair call that has completed:

@@ -58,10 +58,16 @@ class cr_rope(ctypes.Structure):
     _fields_ = [("theta", ctypes.c_double), ("inv_freq", POINTER(c_float)), ("scale", c_float)]
 
 
+class cr_kv_pages(ctypes.Structure):
+    _fields_ = [("block_size", c_int32), ("n_blocks", c_int32), ("stride_block", c_int64),
+                ("block_table", POINTER(c_int32))]
+
+
 class cr_options(ctypes.Structure):
     _fields_ = [("mask", c_int32), ("reinject", c_int32), ("residual", c_int32),
                 ("apply", c_int32), ("keep_first_chunk", c_int32),
-                ("global_rope", POINTER(cr_rope)), ("position_offset", POINTER(c_int32))]
+                ("global_rope", POINTER(cr_rope)), ("position_offset", POINTER(c_int32)),
+                ("pages", POINTER(cr_kv_pages))]
 
 
 class cr_kernel_stat(ctypes.Structure):
@@ -105,8 +111,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cr_repair_ex.argtypes = lib.cr_repair.argtypes + [P(cr_options)]
     lib.cr_rotate_workspace_bytes.argtypes = [P(cr_kv_layout), c_int64, P(c_uint64)]
     lib.cr_rotate_keys.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
-                                   c_int32, P(cr_rope), P(c_int32), c_int32, c_void_p, c_uint64,
-                                   c_void_p]
+                                   c_int32, P(cr_rope), P(c_int32), c_int32, P(cr_kv_pages),
+                                   c_void_p, c_uint64, c_void_p]
     lib.cr_workspace_view.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, c_char_p,
                                       P(c_uint64), P(c_int64)]
     lib.cr_profile_enable.argtypes = [c_int32]
@@ -206,14 +212,17 @@ class Options:
 
     mask: "block_causal" | "token_causal" | "bidirectional" | "block_diagonal";
     apply: "kv" | "k" | "v"; global_rope: None or dict(theta=..., inv_freq=[...]
-    or None, scale=1.0); position_offset: None or one int per request.
+    or None, scale=1.0); position_offset: None or one int per request;
+    pages: None or dict(block_size=..., n_blocks=..., stride_block=...,
+    block_table=[...]) (see pages_struct).
     """
 
     def __init__(self, mask="block_causal", reinject=True, residual=True, apply="kv",
-                 keep_first_chunk=False, global_rope=None, position_offset=None):
+                 keep_first_chunk=False, global_rope=None, position_offset=None, pages=None):
         self.mask, self.reinject, self.residual = mask, reinject, residual
         self.apply, self.keep_first_chunk = apply, keep_first_chunk
         self.global_rope, self.position_offset = global_rope, position_offset
+        self.pages = pages
 
     def to_c(self):
         """(cr_options, keep-alive list) for one call."""
@@ -233,8 +242,21 @@ class Options:
             po = np.ascontiguousarray(self.position_offset, dtype=np.int32)
             keep.append(po)
             o.position_offset = po.ctypes.data_as(POINTER(c_int32))
+        if self.pages is not None:
+            pg, k = pages_struct(**self.pages)
+            keep += [pg, k]
+            o.pages = ctypes.pointer(pg)
         keep.append(o)
         return o, keep
+
+
+def pages_struct(block_size, n_blocks, stride_block, block_table):
+    """(cr_kv_pages, keep-alive) for a paged cache layout (host block table)."""
+    t = np.ascontiguousarray(block_table, dtype=np.int32)
+    pg = cr_kv_pages()
+    pg.block_size, pg.n_blocks, pg.stride_block = int(block_size), int(n_blocks), int(stride_block)
+    pg.block_table = t.ctypes.data_as(POINTER(c_int32))
+    return pg, t
 
 
 def rope_struct(theta=1e4, inv_freq=None, scale=1.0):
@@ -274,16 +296,21 @@ def cr_rotate_workspace_bytes(layout: cr_kv_layout, n_tokens: int) -> int:
 def cr_rotate_keys(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
                    request_chunks: Optional[Sequence[int]], rope: dict,
                    position_offset: Optional[Sequence[int]], inverse: bool, workspace: int,
-                   workspace_bytes: int, stream: Optional[int] = None) -> None:
+                   workspace_bytes: int, stream: Optional[int] = None,
+                   pages: Optional[dict] = None) -> None:
     off, m = _i32(chunk_offsets)
     req, r = _i32(request_chunks)
     rs, keep = rope_struct(**rope)
     po = None if position_offset is None else np.ascontiguousarray(position_offset, np.int32)
+    pg = None
+    if pages is not None:
+        pg, kt = pages_struct(**pages)
     _check(load().cr_rotate_keys(
         kv, ctypes.byref(layout), off.ctypes.data_as(POINTER(c_int32)), m,
         req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r, ctypes.byref(rs),
         po.ctypes.data_as(POINTER(c_int32)) if po is not None else None, int(inverse),
-        workspace, workspace_bytes, stream), "cr_rotate_keys")
+        ctypes.byref(pg) if pg is not None else None, workspace, workspace_bytes, stream),
+        "cr_rotate_keys")
     del keep
 
 
@@ -314,6 +341,16 @@ def cr_profile_read() -> List[dict]:
 def make_dims(d_model, d_seg, d_c, d_b, n_blocks, n_heads, ffn_mult, rope_theta=1e4,
               ln_eps=1e-5) -> cr_dims:
     return cr_dims(d_model, d_seg, d_c, d_b, n_blocks, n_heads, ffn_mult, rope_theta, ln_eps)
+
+
+def paged_layout(n_layers, n_kv_heads, head_dim, n_blocks, block_size, dtype):
+    """(cr_kv_layout, stride_block) of a contiguous [L][2][n_blocks][block_size][H][d_h]
+    block pool."""
+    sH = head_dim
+    sT = n_kv_heads * head_dim
+    sB = block_size * sT
+    sKV = n_blocks * sB
+    return cr_kv_layout(n_layers, n_kv_heads, head_dim, dtype, 2 * sKV, sKV, sT, sH), sB
 
 
 def layer_major_layout(n_layers, n_kv_heads, head_dim, n_tokens, dtype) -> cr_kv_layout:

@@ -86,6 +86,44 @@ cr_status check_layout(const cr_kv_layout* l, int64_t n_tokens) {
   return CR_OK;
 }
 
+// Injectivity of a paged layout over (layer, kv, block, row, head, dim) and
+// validity of the host block table for n_tokens tokens.
+cr_status check_pages(const cr_kv_layout* l, const cr_kv_pages* pg, int64_t n_tokens) {
+  const int bs = pg->block_size;
+  if (bs < 1 || bs > 1024 || (bs & (bs - 1)) || pg->n_blocks < 1) return CR_ERR_LAYOUT;
+  if (pg->stride_block < 0 || pg->stride_block % 8) return CR_ERR_LAYOUT;
+  const int64_t st[5] = {l->stride_layer, l->stride_kv, pg->stride_block, l->stride_token,
+                         l->stride_head};
+  const int64_t ext[5] = {l->n_layers, 2, pg->n_blocks, bs, l->n_kv_heads};
+  struct D { int64_t s, e; };
+  std::vector<D> dims{{1, l->head_dim}};
+  for (int i = 0; i < 5; ++i) {
+    if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
+    if (ext[i] > 1) dims.push_back({st[i], ext[i]});
+  }
+  std::sort(dims.begin(), dims.end(), [](const D& a, const D& b) { return a.s < b.s; });
+  int64_t reach = 0;
+  for (const D& x : dims) {
+    if (x.s <= reach) return CR_ERR_LAYOUT;
+    reach += x.s * (x.e - 1);
+  }
+  const int64_t nb = (n_tokens + bs - 1) / bs;
+  if (nb == 0) return CR_OK;
+  if (!pg->block_table) return CR_ERR_NULL;
+  std::vector<int32_t> ids(pg->block_table, pg->block_table + nb);
+  for (int32_t b : ids)
+    if (b < 0 || b >= pg->n_blocks) return CR_ERR_LAYOUT;
+  std::sort(ids.begin(), ids.end());
+  if (std::adjacent_find(ids.begin(), ids.end()) != ids.end()) return CR_ERR_LAYOUT;
+  return CR_OK;
+}
+
+int log2_int(int x) {
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return s;
+}
+
 cr_status check_offsets(const int32_t* off, int32_t n_chunks, const int32_t* req,
                         int32_t n_req) {
   if (!off) return CR_ERR_NULL;
@@ -241,7 +279,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
 
 struct Workspace {
   int64_t n, n_pad, ldst, ldinj;
-  uint64_t lo, hi, pos, gpos, flags, rope, krope, U, st, inj, h, a, q, k, vt, o, f, total;
+  uint64_t lo, hi, pos, gpos, flags, blocks, rope, krope, U, st, inj, h, a, q, k, vt, o, f, total;
 };
 
 Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
@@ -257,6 +295,7 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   Arena a;
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
   w.gpos = a.take(N * 4); w.flags = a.take(N * 4);
+  w.blocks = a.take(N * 4);                           // device copy of a paged block table
   w.rope = a.take(std::max<int64_t>(N, 1) * (dhd / 2) * 8);
   w.krope = a.take(N * (l->head_dim / 2) * 8);        // global key placement table
   w.U = a.take(N * kc_pad * T);
@@ -390,6 +429,7 @@ struct CallOpts {
   bool place_keys = false;
   cr::KeyRope kr{};
   const int32_t* pos_offset = nullptr;
+  const cr_kv_pages* pages = nullptr;
 };
 
 template <typename T>
@@ -418,9 +458,18 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
     *k = WT(W.k), *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
   const int64_t ldinj = W.ldinj;
   const int B = d->n_blocks;
-  const cr::KvStrides ks{l->stride_layer, l->stride_kv, l->stride_token, l->stride_head,
-                         l->n_kv_heads, l->head_dim};
+  cr::KvStrides ks{l->stride_layer, l->stride_kv, l->stride_token, l->stride_head,
+                   l->n_kv_heads, l->head_dim};
   const float eps = d->ln_eps;
+  if (opt.pages) {
+    int* blocks = reinterpret_cast<int*>(ws + W.blocks);
+    const int nb = (int)((N + opt.pages->block_size - 1) / opt.pages->block_size);
+    CR_TRY(timed("block_table", s, [&] {
+        return cr::copy_table(opt.pages->block_table, nb, blocks, s); }));
+    ks.blocks = blocks;
+    ks.block_shift = log2_int(opt.pages->block_size);
+    ks.block = opt.pages->stride_block;
+  }
 
   CR_TRY(timed("schedule", s, [&] {
       return cr::chunk_schedule(off, n_chunks, req, n_req, opt.mask, opt.pos_offset, lo, hi, pos,
@@ -611,6 +660,7 @@ void cr_default_options(cr_options* opt) {
   opt->keep_first_chunk = 0;
   opt->global_rope = nullptr;
   opt->position_offset = nullptr;
+  opt->pages = nullptr;
 }
 
 cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
@@ -648,7 +698,12 @@ cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chun
   }
   const int64_t N = chunk_offsets[n_chunks];
   if (N >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
-  st = check_layout(layout, N);
+  if (o.pages) {
+    st = check_pages(layout, o.pages, N);
+    opt.pages = o.pages;
+  } else {
+    st = check_layout(layout, N);
+  }
   if (st != CR_OK) return st;
   if (!aligned(kv, 16) || !aligned(token_embeds, 16)) return CR_ERR_LAYOUT;
   if (prepared_bytes < prepared_layout(dims, layout).total || !aligned(prepared, ALIGN))
@@ -690,9 +745,10 @@ cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_o
                       stream, &o);
 }
 
-// workspace of cr_rotate_keys: lo, hi, pos, gpos (int32 each) and the table
+// workspace of cr_rotate_keys: lo, hi, pos, gpos, block table (int32 each)
+// and the (cos, sin) table
 static uint64_t rotate_ws_bytes(const cr_kv_layout* l, int64_t N) {
-  return align_up(4 * (uint64_t)N * 4) + align_up((uint64_t)N * (l->head_dim / 2) * 8);
+  return align_up(5 * (uint64_t)N * 4) + align_up((uint64_t)N * (l->head_dim / 2) * 8);
 }
 
 cr_status cr_rotate_workspace_bytes(const cr_kv_layout* layout, int64_t n_tokens,
@@ -707,7 +763,8 @@ cr_status cr_rotate_workspace_bytes(const cr_kv_layout* layout, int64_t n_tokens
 cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
                          int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
                          const cr_rope* rope, const int32_t* position_offset, int32_t inverse,
-                         void* workspace, uint64_t workspace_bytes, void* stream) {
+                         const cr_kv_pages* pages, void* workspace, uint64_t workspace_bytes,
+                         void* stream) {
   if (!kv || !layout || !rope || !workspace) return CR_ERR_NULL;
   if (layout->n_layers < 1 || layout->n_kv_heads < 1 || layout->head_dim < 32 ||
       layout->head_dim > 256 || layout->head_dim % 32)
@@ -723,7 +780,7 @@ cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout, const int32_t* ch
   if (st != CR_OK) return st;
   const int64_t N = chunk_offsets[n_chunks];
   if (N >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
-  st = check_layout(layout, N);
+  st = pages ? check_pages(layout, pages, N) : check_layout(layout, N);
   if (st != CR_OK) return st;
   if (!aligned(kv, 16)) return CR_ERR_LAYOUT;
   if (workspace_bytes < rotate_ws_bytes(layout, N) || !aligned(workspace, ALIGN))
@@ -733,9 +790,18 @@ cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout, const int32_t* ch
   if (st != CR_OK) return st;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   int* rows = static_cast<int*>(workspace);
-  float2* tab = reinterpret_cast<float2*>(static_cast<char*>(workspace) + align_up(4 * (uint64_t)N * 4));
-  const cr::KvStrides ks{layout->stride_layer, layout->stride_kv, layout->stride_token,
-                         layout->stride_head, layout->n_kv_heads, layout->head_dim};
+  float2* tab = reinterpret_cast<float2*>(static_cast<char*>(workspace) + align_up(5 * (uint64_t)N * 4));
+  cr::KvStrides ks{layout->stride_layer, layout->stride_kv, layout->stride_token,
+                   layout->stride_head, layout->n_kv_heads, layout->head_dim};
+  if (pages) {
+    int* blocks = rows + 4 * N;
+    if (cr::copy_table(pages->block_table, (int)((N + pages->block_size - 1) / pages->block_size),
+                       blocks, s) != hipSuccess)
+      return CR_ERR_LAUNCH;
+    ks.blocks = blocks;
+    ks.block_shift = log2_int(pages->block_size);
+    ks.block = pages->stride_block;
+  }
   if (cr::chunk_schedule(chunk_offsets, n_chunks, request_chunks, n_requests,
                          CR_MASK_BLOCK_CAUSAL, position_offset, rows, rows + N, rows + 2 * N,
                          rows + 3 * N, nullptr, s) != hipSuccess)

@@ -250,7 +250,7 @@ struct EpiExpand {
     for (int q = 0; q < S::PASSES; ++q) {
       const int gm = m0 + S::row(q);
       p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
-      if (gm < M && (mode & EXPAND_RESIDUAL)) p.x[q].load(base + (int64_t)gm * ks.token);
+      if (gm < M && (mode & EXPAND_RESIDUAL)) p.x[q].load(base + ks.tok(gm));
     }
   }
   template <int ROWS, int COLS, int LDC>
@@ -270,7 +270,7 @@ struct EpiExpand {
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + p.sg[e] * (a[e] + p.b[e]);
       p.x[q].from_float(f);
-      p.x[q].store(base + (int64_t)gm * ks.token);
+      p.x[q].store(base + ks.tok(gm));
     }
   }
 };
@@ -320,8 +320,9 @@ struct EpiExpandRope {
       const int gm = m0 + threadIdx.x / Map<COLS>::PAIRS + q * Map<COLS>::RSTEP;
       p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
       if (gm < M) {
-        p.x1[q].load(k.b1 + (int64_t)gm * ks.token);
-        p.x2[q].load(k.b1 + half + (int64_t)gm * ks.token);
+        const int64_t to = ks.tok(gm);
+        p.x1[q].load(k.b1 + to);
+        p.x2[q].load(k.b1 + half + to);
       }
     }
   }
@@ -379,8 +380,9 @@ struct EpiExpandRope {
       }
       p.x1[q].from_float(y1);
       p.x2[q].from_float(y2);
-      p.x1[q].store(k.b1 + (int64_t)gm * ks.token);
-      p.x2[q].store(k.b1 + half + (int64_t)gm * ks.token);
+      const int64_t to = ks.tok(gm);
+      p.x1[q].store(k.b1 + to);
+      p.x2[q].store(k.b1 + half + to);
     }
     }
   }

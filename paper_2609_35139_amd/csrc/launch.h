@@ -26,11 +26,25 @@ LaunchEvents& launch_events();
     le_.start = nullptr;                                                                \
   } while (0)
 
-// Cache layout as seen by the kernels (elements).
+// Cache layout as seen by the kernels (elements).  Strided: token t at
+// t*token.  Paged (blocks != null): token t in block blocks[t >> block_shift]
+// at row t & (2^block_shift - 1), i.e. blocks[..]*block + row*token.
 struct KvStrides {
   int64_t layer, kv, token, head;
   int n_kv_heads, head_dim;
+  const int* blocks = nullptr;
+  int block_shift = 0;
+  int64_t block = 0;
+  __device__ __forceinline__ int64_t tok(int t) const {
+    if (blocks)
+      return (int64_t)blocks[t >> block_shift] * block + (int64_t)(t & ((1 << block_shift) - 1)) * token;
+    return (int64_t)t * token;
+  }
 };
+
+// ---- block table of a paged cache copied from host to device memory
+// (passed by value in batches; no host-side staging buffer).
+hipError_t copy_table(const int32_t* host, int n, int* dev, hipStream_t s);
 
 // ---- GEMM: C[M][N] = A[M][K] * B[N][K]^T, fp32 accumulation, K % 64 == 0.
 // Bias / GELU / residual epilogue: out = (resid +) act(acc + bias) (+ resid2).

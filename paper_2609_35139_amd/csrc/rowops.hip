@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void compress_segments_kernel(
   frag a[NK], w[2][NK];
 #pragma unroll
   for (int k = 0; k < NK; ++k)
-    a[k] = tr < N ? load_frag<T, frag>(base + (int64_t)tr * ks.token + k * MM::KSTEP + fk) : frag{};
+    a[k] = tr < N ? load_frag<T, frag>(base + ks.tok(tr) + k * MM::KSTEP + fk) : frag{};
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -238,6 +238,29 @@ hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* r
   return hipSuccess;
 }
 
+// ----------------------------------------------------- paged block table
+constexpr int TABLE_BATCH = 512;
+struct TableBatch {
+  int count;
+  int v[TABLE_BATCH];
+};
+
+__global__ __launch_bounds__(256) void table_kernel(TableBatch tb, int* __restrict__ dst) {
+  for (int i = threadIdx.x; i < tb.count; i += 256) dst[i] = tb.v[i];
+}
+
+hipError_t copy_table(const int32_t* host, int n, int* dev, hipStream_t s) {
+  for (int i0 = 0; i0 < n; i0 += TABLE_BATCH) {
+    TableBatch tb;
+    tb.count = std::min(TABLE_BATCH, n - i0);
+    for (int i = 0; i < tb.count; ++i) tb.v[i] = host[i0 + i];
+    CR_LAUNCH(table_kernel, dim3(1), dim3(256), 0, s, tb, dev + i0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 // ------------------------------------------------- target-model key rotation
 // tab[t][i] = scale * (cos, sin)(gpos[t] * f_i), angles and cosines in fp64.
 __global__ __launch_bounds__(256) void key_rope_table_kernel(float2* __restrict__ tab,
@@ -277,7 +300,7 @@ __global__ __launch_bounds__(256) void rotate_keys_kernel(T* __restrict__ kv, Kv
   rem /= per_head;
   const int h = rem % ks.n_kv_heads, l = rem / ks.n_kv_heads;
   const int i0 = seg8 * 8;
-  T* p1 = kv + (int64_t)l * ks.layer + (int64_t)t * ks.token + (int64_t)h * ks.head + i0;
+  T* p1 = kv + (int64_t)l * ks.layer + ks.tok(t) + (int64_t)h * ks.head + i0;
   T* p2 = p1 + half;
   Vec8<T> a, b;
   a.load(p1);

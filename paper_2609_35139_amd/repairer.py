@@ -95,12 +95,13 @@ class Repairer:
                     request_chunks: Optional[Sequence[int]], rope: dict,
                     position_offset: Optional[Sequence[int]] = None, inverse: bool = False,
                     layout: Optional[B.cr_kv_layout] = None,
-                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+                    stream: Optional[torch.cuda.Stream] = None,
+                    pages: Optional[dict] = None) -> torch.Tensor:
         """K <- R_M(p)^(+-1) K in place for every token (cr_rotate_keys)."""
         n = int(chunk_offsets[-1])
         lay = layout if layout is not None else self.layout(n)
         nb = B.cr_rotate_workspace_bytes(lay, n)
         ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=self.device)
         B.cr_rotate_keys(kv.data_ptr(), lay, chunk_offsets, request_chunks, rope, position_offset,
-                         inverse, ws.data_ptr(), ws.numel(), _stream_handle(stream))
+                         inverse, ws.data_ptr(), ws.numel(), _stream_handle(stream), pages=pages)
         return kv

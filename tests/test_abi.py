@@ -180,11 +180,12 @@ def test_workspace_views():
 # ------------------------------------------------------------- variants
 def test_option_structs_and_defaults():
     assert ctypes.sizeof(B.cr_rope) == 24
-    assert ctypes.sizeof(B.cr_options) == 40
+    assert ctypes.sizeof(B.cr_options) == 48
+    assert ctypes.sizeof(B.cr_kv_pages) == 24
     o = B.cr_options()
     B.load().cr_default_options(ctypes.byref(o))
     assert (o.mask, o.reinject, o.residual, o.apply, o.keep_first_chunk) == (0, 1, 1, 0, 0)
-    assert not o.global_rope and not o.position_offset
+    assert not o.global_rope and not o.position_offset and not o.pages
 
 
 def _call_repair_ex(w, options, layout=None, dims=None):
@@ -263,3 +264,52 @@ def test_rotate_keys_validation():
     # an empty batch returns before touching the device
     _call_rotate(W0, offsets=np.array([0, 0]), layout=_layout(W0, n=0))
     assert B.cr_rotate_workspace_bytes(_layout(W0), 100) >= 100 * 16 + 100 * W0.target.head_dim * 4
+
+
+# ------------------------------------------------------------- paged cache
+def _paged(w, bs=16, extra=3, table=None, stride_block=None, n_blocks=None):
+    t = w.target
+    nb_tok = -(-w.n_tokens // bs)
+    nbl = nb_tok + extra if n_blocks is None else n_blocks
+    lay, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, nbl, bs,
+                             B.CR_DTYPE_BF16 if w.dtype == "bf16" else B.CR_DTYPE_F32)
+    tab = list(range(nbl))[::-1][:nb_tok] if table is None else table
+    return lay, dict(block_size=bs, n_blocks=nbl, stride_block=sB if stride_block is None
+                     else stride_block, block_table=tab)
+
+
+@pytest.mark.parametrize("change", ["bs3", "bs2048", "nblocks0", "out_of_range", "negative",
+                                    "duplicate", "overlap", "odd_stride"])
+def test_bad_pages(change):
+    w = W0
+    lay, pg = _paged(w)
+    nb = len(pg["block_table"])
+    if change == "bs3":
+        pg["block_size"] = 3
+    elif change == "bs2048":
+        pg["block_size"] = 2048
+    elif change == "nblocks0":
+        pg["n_blocks"] = 0
+    elif change == "out_of_range":
+        pg["block_table"] = [pg["n_blocks"]] + pg["block_table"][1:]
+    elif change == "negative":
+        pg["block_table"] = [-1] + pg["block_table"][1:]
+    elif change == "duplicate":
+        pg["block_table"] = [pg["block_table"][0]] * nb
+    elif change == "overlap":
+        pg["stride_block"] = lay.stride_token      # blocks alias rows
+    elif change == "odd_stride":
+        pg["stride_block"] += 4
+    assert _call_repair_ex(w, B.Options(pages=pg), layout=lay) == "CR_ERR_LAYOUT"
+    with pytest.raises(B.CrError) as e:
+        B.cr_rotate_keys(0x10000, lay, w.chunk_offsets, w.request_chunks, dict(theta=1e4), None,
+                         0, 0x40000, B.cr_rotate_workspace_bytes(lay, w.n_tokens), None, pages=pg)
+    assert e.value.name == "CR_ERR_LAYOUT"
+
+
+def test_valid_pages_pass_host_validation():
+    """A valid paged layout is accepted up to the device check (N == 0 returns OK)."""
+    lay, pg = _paged(W0)
+    B.cr_repair_ex(0x10000, lay, np.array([0, 0]), None, 0x20000, _dims(W0), 0x30000,
+                   B.cr_prepared_bytes(_dims(W0), lay), 0x40000,
+                   B.cr_workspace_bytes(_dims(W0), lay, 0), None, B.Options(pages=pg))
