@@ -265,6 +265,13 @@ typedef struct {
  *                    position of t within its request.  Each p_t must be
  *                    non-negative and below 2^31 - 1.
  *  pages:            NULL, or a paged cache layout (cr_kv_pages).
+ *  kv_out, layout_out, pages_out: when kv_out is not NULL the repaired cache
+ *                    is written there (device, layout_out with the same
+ *                    n_layers, n_kv_heads, head_dim and dtype as layout,
+ *                    optionally paged) and kv is only read: the write into
+ *                    the serving cache is fused into the output add.  Every
+ *                    coordinate of tokens [0, N) of kv_out is written; kv_out
+ *                    must not overlap kv, token_embeds or the workspace.
  */
 /*
  * Paged cache (the block-table layout of paged serving caches; the paper's
@@ -301,6 +308,9 @@ typedef struct {
     const cr_rope* global_rope;
     const int32_t* position_offset;
     const cr_kv_pages* pages;    /* NULL = the strided layout of cr_kv_layout */
+    void* kv_out;                    /* NULL = repair in place                 */
+    const cr_kv_layout* layout_out;  /* layout of kv_out (required with it)    */
+    const cr_kv_pages* pages_out;    /* NULL = strided layout_out              */
 } cr_options;
 
 /* Fills opt with the method's options. */
@@ -341,6 +351,61 @@ CR_API cr_status cr_rotate_keys(void* kv, const cr_kv_layout* layout,
                          const cr_rope* rope, const int32_t* position_offset,
                          int32_t inverse, const cr_kv_pages* pages,
                          void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * Pipelined repair of a sequence of requests whose stale caches sit in
+ * pinned host memory (the transfer is the largest TTFT component for the
+ * larger targets, Table tab:repair-latency-components, "H2D"; overlapping it
+ * with repair across requests is the paper's stated next step).  Request i
+ * is copied host -> device into staging slot i % 2 on copy_stream while
+ * request i - 1 is repaired on compute_stream from the other slot, straight
+ * into its destination cache (out of place, optionally paged).  Events of
+ * the handle order the two streams; a slot is refilled only after the
+ * repair that read it has finished, also across calls on one handle.  The
+ * host buffers must stay valid until copy_stream has passed the copies;
+ * each destination is complete once compute_stream has passed the call.
+ *
+ * cr_pipeline_create / cr_pipeline_destroy: the handle holds four HIP events
+ * (created here, never inside cr_repair_pipelined).  A handle serves one
+ * cr_repair_pipelined call at a time.
+ * cr_pipeline_staging_bytes: device staging for two slots of max_tokens
+ * tokens (cache [L][2][n][H][d_h] and embeddings [n][d_model]).
+ */
+typedef struct {
+    const void* kv_host;             /* pinned host, stale canonical cache, layer-major
+                                        [L][2][n][H][d_h], n = chunk_offsets[n_chunks] */
+    const void* embeds_host;         /* pinned host, [n][d_model]                    */
+    const int32_t* chunk_offsets;    /* host, n_chunks+1 token offsets (one request) */
+    int32_t n_chunks;
+    int32_t position_offset;         /* global position of the first token (with
+                                        options->global_rope)                       */
+    void* kv_out;                    /* device destination cache                     */
+    const cr_kv_layout* layout_out;  /* its layout (n = its token extent)            */
+    const cr_kv_pages* pages_out;    /* NULL = strided                               */
+} cr_pipeline_item;
+
+typedef struct cr_pipeline_s* cr_pipeline;
+
+CR_API cr_status cr_pipeline_create(cr_pipeline* pipeline);
+CR_API cr_status cr_pipeline_destroy(cr_pipeline pipeline);
+CR_API cr_status cr_pipeline_staging_bytes(const cr_dims* dims, const cr_kv_layout* layout,
+                                    int64_t max_tokens, uint64_t* bytes);
+/*
+ * items: host array of n_items requests, each at most max_tokens tokens.
+ * layout: n_layers, n_kv_heads, head_dim and dtype of every request's cache
+ * (strides ignored).  staging, workspace: device, cr_pipeline_staging_bytes
+ * and cr_workspace_bytes for max_tokens, 256-byte aligned.  options: the
+ * variant (its pages, kv_out, layout_out, pages_out and position_offset are
+ * ignored: they come from the items), or NULL for the method.
+ * copy_stream and compute_stream must be distinct.  Validation of every
+ * item happens before anything is enqueued.
+ */
+CR_API cr_status cr_repair_pipelined(cr_pipeline pipeline, const cr_pipeline_item* items,
+                              int32_t n_items, const cr_dims* dims, const cr_kv_layout* layout,
+                              const void* prepared, uint64_t prepared_bytes, void* staging,
+                              uint64_t staging_bytes, int64_t max_tokens, void* workspace,
+                              uint64_t workspace_bytes, const cr_options* options,
+                              void* copy_stream, void* compute_stream);
 
 /*
  * Debug view into the workspace after a cr_repair call that has completed:

@@ -30,7 +30,8 @@ STATUS = {
 EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_bytes",
            "cr_prepare_weights", "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair",
            "cr_default_options", "cr_repair_ex", "cr_rotate_workspace_bytes", "cr_rotate_keys",
-           "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]
+           "cr_pipeline_create", "cr_pipeline_destroy", "cr_pipeline_staging_bytes",
+           "cr_repair_pipelined", "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]
 CR_MASK = {"block_causal": 0, "token_causal": 1, "bidirectional": 2, "block_diagonal": 3}
 CR_APPLY = {"kv": 0, "k": 1, "v": 2}
 
@@ -67,7 +68,15 @@ class cr_options(ctypes.Structure):
     _fields_ = [("mask", c_int32), ("reinject", c_int32), ("residual", c_int32),
                 ("apply", c_int32), ("keep_first_chunk", c_int32),
                 ("global_rope", POINTER(cr_rope)), ("position_offset", POINTER(c_int32)),
-                ("pages", POINTER(cr_kv_pages))]
+                ("pages", POINTER(cr_kv_pages)), ("kv_out", c_void_p),
+                ("layout_out", POINTER(cr_kv_layout)), ("pages_out", POINTER(cr_kv_pages))]
+
+
+class cr_pipeline_item(ctypes.Structure):
+    _fields_ = [("kv_host", c_void_p), ("embeds_host", c_void_p),
+                ("chunk_offsets", POINTER(c_int32)), ("n_chunks", c_int32),
+                ("position_offset", c_int32), ("kv_out", c_void_p),
+                ("layout_out", POINTER(cr_kv_layout)), ("pages_out", POINTER(cr_kv_pages))]
 
 
 class cr_kernel_stat(ctypes.Structure):
@@ -113,14 +122,22 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cr_rotate_keys.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
                                    c_int32, P(cr_rope), P(c_int32), c_int32, P(cr_kv_pages),
                                    c_void_p, c_uint64, c_void_p]
+    lib.cr_pipeline_create.argtypes = [P(c_void_p)]
+    lib.cr_pipeline_destroy.argtypes = [c_void_p]
+    lib.cr_pipeline_staging_bytes.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, P(c_uint64)]
+    lib.cr_repair_pipelined.argtypes = [c_void_p, P(cr_pipeline_item), c_int32, P(cr_dims),
+                                        P(cr_kv_layout), c_void_p, c_uint64, c_void_p, c_uint64,
+                                        c_int64, c_void_p, c_uint64, P(cr_options), c_void_p,
+                                        c_void_p]
     lib.cr_workspace_view.argtypes = [P(cr_dims), P(cr_kv_layout), c_int64, c_char_p,
                                       P(c_uint64), P(c_int64)]
     lib.cr_profile_enable.argtypes = [c_int32]
     lib.cr_profile_read.argtypes = [P(cr_kernel_stat), c_int32, P(c_int32)]
     for name in ["cr_weights_layout", "cr_prepared_bytes", "cr_prepare_weights",
                  "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_repair_ex",
-                 "cr_rotate_workspace_bytes", "cr_rotate_keys", "cr_workspace_view",
-                 "cr_profile_enable", "cr_profile_read"]:
+                 "cr_rotate_workspace_bytes", "cr_rotate_keys", "cr_pipeline_create",
+                 "cr_pipeline_destroy", "cr_pipeline_staging_bytes", "cr_repair_pipelined",
+                 "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]:
         getattr(lib, name).restype = c_int32
     _lib = lib
     return lib
@@ -218,11 +235,13 @@ class Options:
     """
 
     def __init__(self, mask="block_causal", reinject=True, residual=True, apply="kv",
-                 keep_first_chunk=False, global_rope=None, position_offset=None, pages=None):
+                 keep_first_chunk=False, global_rope=None, position_offset=None, pages=None,
+                 kv_out=None, layout_out=None, pages_out=None):
         self.mask, self.reinject, self.residual = mask, reinject, residual
         self.apply, self.keep_first_chunk = apply, keep_first_chunk
         self.global_rope, self.position_offset = global_rope, position_offset
         self.pages = pages
+        self.kv_out, self.layout_out, self.pages_out = kv_out, layout_out, pages_out
 
     def to_c(self):
         """(cr_options, keep-alive list) for one call."""
@@ -246,6 +265,15 @@ class Options:
             pg, k = pages_struct(**self.pages)
             keep += [pg, k]
             o.pages = ctypes.pointer(pg)
+        if self.kv_out is not None:
+            o.kv_out = self.kv_out
+            if self.layout_out is not None:
+                keep.append(self.layout_out)
+                o.layout_out = ctypes.pointer(self.layout_out)
+            if self.pages_out is not None:
+                pg, k = pages_struct(**self.pages_out)
+                keep += [pg, k]
+                o.pages_out = ctypes.pointer(pg)
         keep.append(o)
         return o, keep
 
@@ -311,6 +339,60 @@ def cr_rotate_keys(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
         po.ctypes.data_as(POINTER(c_int32)) if po is not None else None, int(inverse),
         ctypes.byref(pg) if pg is not None else None, workspace, workspace_bytes, stream),
         "cr_rotate_keys")
+    del keep
+
+
+def cr_pipeline_create() -> int:
+    h = c_void_p()
+    _check(load().cr_pipeline_create(ctypes.byref(h)), "cr_pipeline_create")
+    return h.value
+
+
+def cr_pipeline_destroy(handle: int) -> None:
+    _check(load().cr_pipeline_destroy(handle), "cr_pipeline_destroy")
+
+
+def cr_pipeline_staging_bytes(dims: cr_dims, layout: cr_kv_layout, max_tokens: int) -> int:
+    b = c_uint64(0)
+    _check(load().cr_pipeline_staging_bytes(ctypes.byref(dims), ctypes.byref(layout), max_tokens,
+                                            ctypes.byref(b)), "cr_pipeline_staging_bytes")
+    return b.value
+
+
+def cr_repair_pipelined(handle: int, items: Sequence[dict], dims: cr_dims, layout: cr_kv_layout,
+                        prepared: int, prepared_bytes: int, staging: int, staging_bytes: int,
+                        max_tokens: int, workspace: int, workspace_bytes: int,
+                        options: Optional[Options], copy_stream: Optional[int],
+                        compute_stream: Optional[int]) -> None:
+    """items: dicts with kv_host, embeds_host (pinned host addresses),
+    chunk_offsets, position_offset (int), kv_out (device address), layout_out
+    (cr_kv_layout), pages_out (None or a pages dict)."""
+    arr = (cr_pipeline_item * max(1, len(items)))()
+    keep = []
+    for i, it in enumerate(items):
+        off = np.ascontiguousarray(it["chunk_offsets"], dtype=np.int32)
+        lay = it["layout_out"]
+        keep += [off, lay]
+        arr[i].kv_host = it["kv_host"]
+        arr[i].embeds_host = it["embeds_host"]
+        arr[i].chunk_offsets = off.ctypes.data_as(POINTER(c_int32))
+        arr[i].n_chunks = len(off) - 1
+        arr[i].position_offset = int(it.get("position_offset", 0))
+        arr[i].kv_out = it["kv_out"]
+        arr[i].layout_out = ctypes.pointer(lay)
+        if it.get("pages_out") is not None:
+            pg, k = pages_struct(**it["pages_out"])
+            keep += [pg, k]
+            arr[i].pages_out = ctypes.pointer(pg)
+    o = None
+    if options is not None:
+        o, k = options.to_c()
+        keep.append(k)
+    _check(load().cr_repair_pipelined(handle, arr, len(items), ctypes.byref(dims),
+                                      ctypes.byref(layout), prepared, prepared_bytes, staging,
+                                      staging_bytes, max_tokens, workspace, workspace_bytes,
+                                      ctypes.byref(o) if o is not None else None, copy_stream,
+                                      compute_stream), "cr_repair_pipelined")
     del keep
 
 

@@ -5,6 +5,7 @@ atomically replaces the library next to this file.
 """
 import concurrent.futures
 import os
+import re
 import subprocess
 import sys
 
@@ -38,19 +39,49 @@ def _run(cmd):
     return out
 
 
+RESOURCES = os.path.join(HERE, "_build", "kernel_resources.txt")
+
+
+def _resources(remarks):
+    """(kernel, VGPRs, scratch bytes per lane, waves per SIMD) from the
+    compiler's kernel-resource-usage remarks."""
+    rows, cur = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"remark:\s+(Function Name|VGPRs|ScratchSize \[bytes/lane\]|"
+                      r"Occupancy \[waves/SIMD\]):\s+(\S+)", line)
+        if not m:
+            continue
+        key, val = m.group(1), m.group(2)
+        if key == "Function Name":
+            cur = {"kernel": val}
+            rows.append(cur)
+        elif cur is not None:
+            cur[key.split()[0]] = int(val)
+    return rows
+
+
 def build(verbose: bool = False) -> str:
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        jobs.append(([_hipcc(), *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src),
-                      "-o", obj], obj))
+        jobs.append(([_hipcc(), *CFLAGS, *EXTRA.get(src, []), "-Rpass-analysis=kernel-resource-usage",
+                      "-c", os.path.join(CSRC, src), "-o", obj], obj))
     workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", "4"))))
+    rows = []
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
         for out in ex.map(_run, [j[0] for j in jobs]):
-            if verbose and out.strip():
-                print(out)
+            rows += _resources(out)
+            rest = "\n".join(l for l in out.splitlines() if "kernel-resource-usage" not in l)
+            if verbose and rest.strip():
+                print(rest)
+    # per-kernel register and scratch use of this build (a spill to scratch
+    # memory in a hot kernel is a performance bug the tests look for)
+    with open(RESOURCES, "w") as fh:
+        for r in rows:
+            fh.write("%s vgprs=%s scratch=%s waves=%s\n" % (
+                r["kernel"], r.get("VGPRs"), r.get("ScratchSize"), r.get("Occupancy")))
     tmp = LIB + ".tmp"
     _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-o", tmp, *[j[1] for j in jobs],
           f"-Wl,--version-script={os.path.join(CSRC, 'exports.map')}"])

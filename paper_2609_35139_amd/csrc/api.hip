@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstring>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -279,7 +280,8 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
 
 struct Workspace {
   int64_t n, n_pad, ldst, ldinj;
-  uint64_t lo, hi, pos, gpos, flags, blocks, rope, krope, U, st, inj, h, a, q, k, vt, o, f, total;
+  uint64_t lo, hi, pos, gpos, flags, blocks, blocks_out, rope, krope, U, st, inj, h, a, q, k, vt, o,
+      f, total;
 };
 
 Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
@@ -296,6 +298,7 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
   w.gpos = a.take(N * 4); w.flags = a.take(N * 4);
   w.blocks = a.take(N * 4);                           // device copy of a paged block table
+  w.blocks_out = a.take(N * 4);                       // ... and of the destination's
   w.rope = a.take(std::max<int64_t>(N, 1) * (dhd / 2) * 8);
   w.krope = a.take(N * (l->head_dim / 2) * 8);        // global key placement table
   w.U = a.take(N * kc_pad * T);
@@ -430,6 +433,9 @@ struct CallOpts {
   cr::KeyRope kr{};
   const int32_t* pos_offset = nullptr;
   const cr_kv_pages* pages = nullptr;
+  void* kv_out = nullptr;                 // out of place: destination cache
+  const cr_kv_layout* layout_out = nullptr;
+  const cr_kv_pages* pages_out = nullptr;
 };
 
 template <typename T>
@@ -469,6 +475,22 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
     ks.blocks = blocks;
     ks.block_shift = log2_int(opt.pages->block_size);
     ks.block = opt.pages->stride_block;
+  }
+  T* kv_out = static_cast<T*>(opt.kv_out);
+  cr::KvStrides ks_out{};
+  if (kv_out) {
+    const cr_kv_layout* lo_ = opt.layout_out;
+    ks_out = cr::KvStrides{lo_->stride_layer, lo_->stride_kv, lo_->stride_token, lo_->stride_head,
+                           lo_->n_kv_heads, lo_->head_dim};
+    if (opt.pages_out) {
+      int* blocks = reinterpret_cast<int*>(ws + W.blocks_out);
+      const int nb = (int)((N + opt.pages_out->block_size - 1) / opt.pages_out->block_size);
+      CR_TRY(timed("block_table", s, [&] {
+          return cr::copy_table(opt.pages_out->block_table, nb, blocks, s); }));
+      ks_out.blocks = blocks;
+      ks_out.block_shift = log2_int(opt.pages_out->block_size);
+      ks_out.block = opt.pages_out->stride_block;
+    }
   }
 
   CR_TRY(timed("schedule", s, [&] {
@@ -529,7 +551,7 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   CR_TRY(timed("gemm_expand", s, [&] {
       return cr::gemm_expand<T>(a, db, PT(P.w_out), M, D, db, kv, ks, PF(P.b_out),
                             PF(P.sigma_delta), opt.expand_mode, flags,
-                            opt.place_keys ? krope : nullptr, s); }));
+                            opt.place_keys ? krope : nullptr, kv_out, ks_out, s); }));
   return CR_OK;
 }
 
@@ -661,21 +683,39 @@ void cr_default_options(cr_options* opt) {
   opt->global_rope = nullptr;
   opt->position_offset = nullptr;
   opt->pages = nullptr;
+  opt->kv_out = nullptr;
+  opt->layout_out = nullptr;
+  opt->pages_out = nullptr;
 }
 
-cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
-                       int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
-                       const void* token_embeds, const cr_dims* dims, const void* prepared,
-                       uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
-                       void* stream, const cr_options* options) {
-  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace || !options)
-    return CR_ERR_NULL;
+}  // extern "C"
+
+namespace {
+
+// A validated repair call.
+struct Call {
+  CallOpts opt;
+  int64_t N = 0;
+  int max_len = 0;
+};
+
+bool same_shape(const cr_kv_layout* a, const cr_kv_layout* b) {
+  return a->n_layers == b->n_layers && a->n_kv_heads == b->n_kv_heads &&
+         a->head_dim == b->head_dim && a->dtype == b->dtype;
+}
+
+// Host-side validation of one cr_repair_ex call (nothing is enqueued).
+cr_status validate_call(const void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                        int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                        const void* token_embeds, const cr_dims* dims, const void* prepared,
+                        uint64_t prepared_bytes, const void* workspace, uint64_t workspace_bytes,
+                        const cr_options& o, Call* c) {
+  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace) return CR_ERR_NULL;
   cr_status st = check_dims(dims, layout);
   if (st != CR_OK) return st;
   st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
   if (st != CR_OK) return st;
-  const cr_options& o = *options;
-  CallOpts opt;
+  CallOpts& opt = c->opt;
   if (o.mask < CR_MASK_BLOCK_CAUSAL || o.mask > CR_MASK_BLOCK_DIAGONAL) return CR_ERR_DIMS;
   if ((o.reinject != 0 && o.reinject != 1) || (o.residual != 0 && o.residual != 1) ||
       (o.keep_first_chunk != 0 && o.keep_first_chunk != 1))
@@ -706,13 +746,21 @@ cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chun
   }
   if (st != CR_OK) return st;
   if (!aligned(kv, 16) || !aligned(token_embeds, 16)) return CR_ERR_LAYOUT;
+  if (o.kv_out) {
+    if (!o.layout_out) return CR_ERR_NULL;
+    if (!same_shape(layout, o.layout_out)) return CR_ERR_LAYOUT;
+    st = o.pages_out ? check_pages(o.layout_out, o.pages_out, N) : check_layout(o.layout_out, N);
+    if (st != CR_OK) return st;
+    if (!aligned(o.kv_out, 16) || o.kv_out == kv) return CR_ERR_LAYOUT;
+    opt.kv_out = o.kv_out;
+    opt.layout_out = o.layout_out;
+    opt.pages_out = o.pages_out;
+  }
   if (prepared_bytes < prepared_layout(dims, layout).total || !aligned(prepared, ALIGN))
     return CR_ERR_WORKSPACE;
   if (workspace_bytes < workspace_layout(dims, layout, N).total || !aligned(workspace, ALIGN))
     return CR_ERR_WORKSPACE;
-  if (N == 0) return CR_OK;
-  st = check_device();
-  if (st != CR_OK) return st;
+  c->N = N;
   int max_len = 0;
   if (request_chunks) {
     for (int r = 0; r < n_requests; ++r)
@@ -721,16 +769,181 @@ cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chun
   } else {
     max_len = (int)N;
   }
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  c->max_len = max_len;
+  return CR_OK;
+}
+
+cr_status enqueue_call(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                       int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                       const void* token_embeds, const cr_dims* dims, const void* prepared,
+                       void* workspace, const Call& c, hipStream_t s) {
+  if (c.N == 0) return CR_OK;
   if (layout->dtype == CR_DTYPE_BF16)
     return repair_impl<bf16>(static_cast<bf16*>(kv), layout, chunk_offsets, n_chunks,
                              request_chunks, n_requests, static_cast<const bf16*>(token_embeds),
                              dims, static_cast<const char*>(prepared),
-                             static_cast<char*>(workspace), N, max_len, opt, s);
+                             static_cast<char*>(workspace), c.N, c.max_len, c.opt, s);
   return repair_impl<float>(static_cast<float*>(kv), layout, chunk_offsets, n_chunks,
                             request_chunks, n_requests, static_cast<const float*>(token_embeds),
                             dims, static_cast<const char*>(prepared),
-                            static_cast<char*>(workspace), N, max_len, opt, s);
+                            static_cast<char*>(workspace), c.N, c.max_len, c.opt, s);
+}
+
+// staging of the pipeline: per slot the cache [L][2][n][H][d_h] and the
+// embeddings [n][d_model] of max_tokens tokens
+struct Staging {
+  uint64_t kv_bytes, emb_bytes, slot_bytes;
+};
+Staging staging_layout(const cr_dims* d, const cr_kv_layout* l, int64_t max_tokens) {
+  Staging g;
+  const uint64_t T = esize(l->dtype);
+  g.kv_bytes = align_up((uint64_t)2 * l->n_layers * max_tokens * l->n_kv_heads * l->head_dim * T);
+  g.emb_bytes = align_up((uint64_t)max_tokens * d->d_model * T);
+  g.slot_bytes = g.kv_bytes + g.emb_bytes;
+  return g;
+}
+
+}  // namespace
+
+struct cr_pipeline_s {
+  hipEvent_t copied[2] = {nullptr, nullptr};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  bool used[2] = {false, false};  // done[b] recorded by this or an earlier call
+};
+
+extern "C" {
+
+cr_status cr_repair_ex(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                       int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                       const void* token_embeds, const cr_dims* dims, const void* prepared,
+                       uint64_t prepared_bytes, void* workspace, uint64_t workspace_bytes,
+                       void* stream, const cr_options* options) {
+  if (!options) return CR_ERR_NULL;
+  Call c;
+  cr_status st = validate_call(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
+                               token_embeds, dims, prepared, prepared_bytes, workspace,
+                               workspace_bytes, *options, &c);
+  if (st != CR_OK) return st;
+  if (c.N == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  return enqueue_call(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
+                      token_embeds, dims, prepared, workspace, c,
+                      reinterpret_cast<hipStream_t>(stream));
+}
+
+cr_status cr_pipeline_create(cr_pipeline* pipeline) {
+  if (!pipeline) return CR_ERR_NULL;
+  cr_pipeline p = new (std::nothrow) cr_pipeline_s;
+  if (!p) return CR_ERR_DEVICE;
+  for (int i = 0; i < 2; ++i) {
+    if (hipEventCreateWithFlags(&p->copied[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&p->done[i], hipEventDisableTiming) != hipSuccess) {
+      cr_pipeline_destroy(p);
+      return CR_ERR_DEVICE;
+    }
+  }
+  *pipeline = p;
+  return CR_OK;
+}
+
+cr_status cr_pipeline_destroy(cr_pipeline p) {
+  if (!p) return CR_ERR_NULL;
+  for (int i = 0; i < 2; ++i) {
+    if (p->copied[i]) hipEventDestroy(p->copied[i]);
+    if (p->done[i]) hipEventDestroy(p->done[i]);
+  }
+  delete p;
+  return CR_OK;
+}
+
+cr_status cr_pipeline_staging_bytes(const cr_dims* dims, const cr_kv_layout* layout,
+                                    int64_t max_tokens, uint64_t* bytes) {
+  if (!dims || !layout || !bytes) return CR_ERR_NULL;
+  const cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  if (max_tokens < 0 || max_tokens >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  *bytes = 2 * staging_layout(dims, layout, max_tokens).slot_bytes;
+  return CR_OK;
+}
+
+cr_status cr_repair_pipelined(cr_pipeline pipeline, const cr_pipeline_item* items,
+                              int32_t n_items, const cr_dims* dims, const cr_kv_layout* layout,
+                              const void* prepared, uint64_t prepared_bytes, void* staging,
+                              uint64_t staging_bytes, int64_t max_tokens, void* workspace,
+                              uint64_t workspace_bytes, const cr_options* options,
+                              void* copy_stream, void* compute_stream) {
+  if (!pipeline || !dims || !layout || !staging || !workspace) return CR_ERR_NULL;
+  if (n_items < 0) return CR_ERR_DIMS;
+  if (n_items > 0 && !items) return CR_ERR_NULL;
+  if (copy_stream == compute_stream) return CR_ERR_DIMS;
+  cr_status st = check_dims(dims, layout);
+  if (st != CR_OK) return st;
+  if (max_tokens < 0 || max_tokens >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
+  const Staging g = staging_layout(dims, layout, max_tokens);
+  if (staging_bytes < 2 * g.slot_bytes || !aligned(staging, ALIGN)) return CR_ERR_WORKSPACE;
+  cr_options base;
+  cr_default_options(&base);
+  if (options) base = *options;
+  base.pages = nullptr;
+  // validate every item against its own staging slot before enqueueing anything
+  std::vector<Call> calls(n_items);
+  std::vector<cr_kv_layout> lays(n_items);
+  for (int i = 0; i < n_items; ++i) {
+    const cr_pipeline_item& it = items[i];
+    if (!it.kv_host || !it.embeds_host || !it.chunk_offsets || !it.kv_out || !it.layout_out)
+      return CR_ERR_NULL;
+    st = check_offsets(it.chunk_offsets, it.n_chunks, nullptr, 1);
+    if (st != CR_OK) return st;
+    const int64_t n = it.chunk_offsets[it.n_chunks];
+    if (n > max_tokens) return CR_ERR_WORKSPACE;
+    const int64_t sT = (int64_t)layout->n_kv_heads * layout->head_dim;
+    lays[i] = cr_kv_layout{layout->n_layers, layout->n_kv_heads, layout->head_dim,
+                           layout->dtype, 2 * n * sT, n * sT, sT, layout->head_dim};
+    cr_options o = base;
+    o.kv_out = it.kv_out;
+    o.layout_out = it.layout_out;
+    o.pages_out = it.pages_out;
+    o.position_offset = &it.position_offset;
+    char* slot = static_cast<char*>(staging) + (i & 1) * g.slot_bytes;
+    st = validate_call(slot, &lays[i], it.chunk_offsets, it.n_chunks, nullptr, 1,
+                       slot + g.kv_bytes, dims, prepared, prepared_bytes, workspace,
+                       workspace_bytes, o, &calls[i]);
+    if (st != CR_OK) return st;
+  }
+  if (n_items == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
+  hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+  const uint64_t T = esize(layout->dtype);
+  for (int i = 0; i < n_items; ++i) {
+    const cr_pipeline_item& it = items[i];
+    const int b = i & 1;
+    char* slot = static_cast<char*>(staging) + b * g.slot_bytes;
+    const int64_t n = calls[i].N;
+    // the slot is refilled only after the repair that read it has finished
+    // (in this call or in an earlier one on the same handle)
+    if (pipeline->used[b] && hipStreamWaitEvent(cs, pipeline->done[b], 0) != hipSuccess)
+      return CR_ERR_LAUNCH;
+    const uint64_t kvb = (uint64_t)2 * layout->n_layers * n * layout->n_kv_heads * layout->head_dim * T;
+    const uint64_t eb = (uint64_t)n * dims->d_model * T;
+    if (n > 0) {
+      if (hipMemcpyAsync(slot, it.kv_host, kvb, hipMemcpyHostToDevice, cs) != hipSuccess ||
+          hipMemcpyAsync(slot + g.kv_bytes, it.embeds_host, eb, hipMemcpyHostToDevice, cs) !=
+              hipSuccess)
+        return CR_ERR_LAUNCH;
+    }
+    if (hipEventRecord(pipeline->copied[b], cs) != hipSuccess ||
+        hipStreamWaitEvent(ks, pipeline->copied[b], 0) != hipSuccess)
+      return CR_ERR_LAUNCH;
+    st = enqueue_call(slot, &lays[i], it.chunk_offsets, it.n_chunks, nullptr, 1,
+                      slot + g.kv_bytes, dims, prepared, workspace, calls[i], ks);
+    if (st != CR_OK) return st;
+    if (hipEventRecord(pipeline->done[b], ks) != hipSuccess) return CR_ERR_LAUNCH;
+    pipeline->used[b] = true;
+  }
+  return CR_OK;
 }
 
 cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,

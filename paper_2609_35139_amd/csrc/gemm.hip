@@ -226,6 +226,7 @@ __device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* 
 template <typename T>
 struct EpiExpand {
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
+  T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
   template <int ROWS, int COLS>
   struct Pre {
     float b[8], sg[8];
@@ -242,35 +243,51 @@ struct EpiExpand {
   __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS>;
     const int gn = n0 + S::col();
+    if (gn >= N) return;
     T* base;
-    if (gn >= N || !selected(gn, &base)) return;   // unselected component: left stale
-    load8f(bias + gn, p.b);
-    load8f(sigma + gn, p.sg);
+    const bool sel = selected(gn, &base);
+    if (!sel && !kvo) return;                      // unselected component: left stale in place
+    if (sel) {
+      load8f(bias + gn, p.b);
+      load8f(sigma + gn, p.sg);
+    }
+    const bool need_x = kvo || (mode & EXPAND_RESIDUAL);
 #pragma unroll
     for (int q = 0; q < S::PASSES; ++q) {
       const int gm = m0 + S::row(q);
       p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
-      if (gm < M && (mode & EXPAND_RESIDUAL)) p.x[q].load(base + ks.tok(gm));
+      if (gm < M && need_x) p.x[q].load(base + ks.tok(gm));
     }
   }
   template <int ROWS, int COLS, int LDC>
   __device__ void run(const float* Cs, Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS>;
     const int c = S::col(), gn = n0 + c;
+    if (gn >= N) return;
     T* base;
-    if (gn >= N || !selected(gn, &base)) return;
+    const bool sel = selected(gn, &base);
+    if (!sel && !kvo) return;
+    bool dummy;
+    T* obase = kvo ? kv_coord(kvo, kso, gn, &dummy) : base;
     const bool res = mode & EXPAND_RESIDUAL;
 #pragma unroll
     for (int q = 0; q < S::PASSES; ++q) {
       const int r = S::row(q), gm = m0 + r;
-      if (gm >= M || p.kp[q]) continue;
+      if (gm >= M) continue;
+      // (no reference that selects between the two stride sets: it would pin
+      // the epilogue's arguments to scratch memory)
+      const int64_t to = kvo ? kso.tok(gm) : ks.tok(gm);
+      if (!sel || p.kp[q]) {                       // stale values: copied when out of place
+        if (kvo) p.x[q].store(obase + to);
+        continue;
+      }
       float a[8], f[8];
       load8f(Cs + r * LDC + c, a);
       if (res) p.x[q].to_float(f);
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + p.sg[e] * (a[e] + p.b[e]);
       p.x[q].from_float(f);
-      p.x[q].store(base + ks.tok(gm));
+      p.x[q].store(obase + to);
     }
   }
 };
@@ -283,7 +300,8 @@ struct EpiExpand {
 template <typename T>
 struct EpiExpandRope {
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
-  const float2* rope;   // [M][head_dim/2] scaled (cos, sin)
+  T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
+  const float2* rope;      // [M][head_dim/2] scaled (cos, sin)
   template <int COLS> struct Map {
     static constexpr int PAIRS = COLS / 16;        // 8-pair groups per tile row
     static constexpr int RSTEP = 256 / PAIRS;
@@ -295,7 +313,7 @@ struct EpiExpandRope {
     Vec8<T> x1[P], x2[P];
     int kp[P];
   };
-  struct Cols { int c1, c2, i0; bool is_k, on; T* b1; };
+  struct Cols { int c1, c2, i0; bool is_k, on; T* b1; T* o1; };
   template <int COLS>
   __device__ bool cols(int n0, int N, Cols& k) const {
     const int dh = ks.head_dim, half = dh / 2, sph = half / 8;
@@ -304,9 +322,11 @@ struct EpiExpandRope {
     k.c2 = k.c1 + half;
     if (n0 + k.c2 >= N) return false;
     k.b1 = kv_coord(kv, ks, n0 + k.c1, &k.is_k);
+    bool dummy;
+    k.o1 = kvo ? kv_coord(kvo, kso, n0 + k.c1, &dummy) : k.b1;
     k.i0 = (n0 + k.c1) % dh;
     k.on = mode & (k.is_k ? EXPAND_K : EXPAND_V);
-    return k.on || k.is_k;                         // stale V: nothing to write
+    return k.on || k.is_k || kvo;                  // stale V in place: nothing to write
   }
   template <int ROWS, int COLS>
   __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
@@ -364,7 +384,7 @@ struct EpiExpandRope {
           y1[e] = (res ? y1[e] : 0.f) + p.s1[e] * (a1[e] + p.b1[e]);
           y2[e] = (res ? y2[e] : 0.f) + p.s2[e] * (a2[e] + p.b2[e]);
         }
-      } else if (!k.is_k) {
+      } else if (!k.is_k && !kvo) {
         continue;
       }
       if (k.is_k) {
@@ -380,9 +400,9 @@ struct EpiExpandRope {
       }
       p.x1[q].from_float(y1);
       p.x2[q].from_float(y2);
-      const int64_t to = ks.tok(gm);
-      p.x1[q].store(k.b1 + to);
-      p.x2[q].store(k.b1 + half + to);
+      const int64_t to = kvo ? kso.tok(gm) : ks.tok(gm);
+      p.x1[q].store(k.o1 + to);
+      p.x2[q].store(k.o1 + half + to);
     }
     }
   }
@@ -540,13 +560,14 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
 template <typename T>
 hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K, T* kv,
                        KvStrides ks, const float* bias, const float* sigma, int mode,
-                       const int* keep, const float2* key_rope, hipStream_t s) {
+                       const int* keep, const float2* key_rope, T* kv_out, KvStrides ks_out,
+                       hipStream_t s) {
   if (key_rope) {
     if (ks.head_dim > 128) return hipErrorInvalidValue;
-    EpiExpandRope<T> e{kv, ks, bias, sigma, mode, keep, key_rope};
+    EpiExpandRope<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out, key_rope};
     return launch<T>(A, lda, B, K, M, N, K, e, s);
   }
-  EpiExpand<T> e{kv, ks, bias, sigma, mode, keep};
+  EpiExpand<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out};
   return launch<T>(A, lda, B, K, M, N, K, e, s);
 }
 
@@ -558,7 +579,7 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
                                   int64_t, const float*, const int*, const float2*, hipStream_t); \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides, \
                                      const float*, const float*, int, const int*,               \
-                                     const float2*, hipStream_t);
+                                     const float2*, T*, KvStrides, hipStream_t);
 CR_INST(bf16)
 CR_INST(float)
 #undef CR_INST

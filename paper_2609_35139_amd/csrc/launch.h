@@ -64,17 +64,20 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
 
 // KV residual head fused with the output add into the strided cache, for
 // coordinates j in [0, D_KV) of the selected components:
-//   kv[t, j] = (residual ? kv[t, j] : 0) + sigma[j] * (acc[t, j] + bias[j]).
+//   out[t, j] = (residual ? kv[t, j] : 0) + sigma[j] * (acc[t, j] + bias[j]).
 // mode: EXPAND_RESIDUAL | EXPAND_K | EXPAND_V.  keep (may be null): tokens
-// with keep[t] != 0 are left unchanged.  With key_rope (may be null, table
-// [M][head_dim/2] of scaled (cos, sin), head_dim <= 128) every key head of
-// every token is then rotated by its row of the table, whether or not it
-// received the output.
+// with keep[t] != 0 keep their stale values.  With key_rope (may be null,
+// table [M][head_dim/2] of scaled (cos, sin), head_dim <= 128) every key head
+// of every token is then rotated by its row of the table, whether or not it
+// received the output.  out is kv itself (kv_out null: in place, unselected
+// coordinates untouched) or kv_out in layout ks_out (every coordinate of
+// tokens [0, M) written; kv only read).
 enum { EXPAND_RESIDUAL = 1, EXPAND_K = 2, EXPAND_V = 4 };
 template <typename T>
 hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K, T* kv,
                        KvStrides ks, const float* bias, const float* sigma, int mode,
-                       const int* keep, const float2* key_rope, hipStream_t s);
+                       const int* keep, const float2* key_rope, T* kv_out, KvStrides ks_out,
+                       hipStream_t s);
 
 // ---- flash attention over per-row key intervals [lo, hi); q pre-scaled by
 // log2(e)/sqrt(d_head); k and vt padded to n_pad >= roundup(N, 64) keys.

@@ -91,6 +91,45 @@ class Repairer:
                            options)
         return kv
 
+    def repair_pipelined(self, items, max_tokens: int, copy_stream: torch.cuda.Stream,
+                         compute_stream: torch.cuda.Stream,
+                         options: Optional[B.Options] = None, staging: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None):
+        """cr_repair_pipelined over items (dicts: kv_host / embeds_host pinned
+        torch tensors, chunk_offsets, position_offset, kv_out device tensor,
+        layout_out, pages_out).  Returns (staging, workspace) for reuse."""
+        if getattr(self, "_pipe", None) is None:
+            self._pipe = B.cr_pipeline_create()
+        lay = self.layout(max_tokens)
+        if staging is None:
+            staging = torch.empty(B.cr_pipeline_staging_bytes(self.dims, lay, max_tokens),
+                                  dtype=torch.uint8, device=self.device)
+        if workspace is None:
+            workspace = self.workspace(max_tokens)
+        c_items = []
+        for it in items:
+            if not it["kv_host"].is_pinned() or not it["embeds_host"].is_pinned():
+                raise ValueError("pipelined repair reads pinned host memory")
+            c_items.append(dict(kv_host=it["kv_host"].data_ptr(),
+                                embeds_host=it["embeds_host"].data_ptr(),
+                                chunk_offsets=it["chunk_offsets"],
+                                position_offset=it.get("position_offset", 0),
+                                kv_out=it["kv_out"].data_ptr(), layout_out=it["layout_out"],
+                                pages_out=it.get("pages_out")))
+        B.cr_repair_pipelined(self._pipe, c_items, self.dims, lay, self.prepared.data_ptr(),
+                              self.prepared_bytes, staging.data_ptr(), staging.numel(), max_tokens,
+                              workspace.data_ptr(), workspace.numel(), options,
+                              _stream_handle(copy_stream), _stream_handle(compute_stream))
+        return staging, workspace
+
+    def __del__(self):
+        pipe = getattr(self, "_pipe", None)
+        if pipe:
+            try:
+                B.cr_pipeline_destroy(pipe)
+            except Exception:
+                pass
+
     def rotate_keys(self, kv: torch.Tensor, chunk_offsets: Sequence[int],
                     request_chunks: Optional[Sequence[int]], rope: dict,
                     position_offset: Optional[Sequence[int]] = None, inverse: bool = False,

@@ -180,12 +180,13 @@ def test_workspace_views():
 # ------------------------------------------------------------- variants
 def test_option_structs_and_defaults():
     assert ctypes.sizeof(B.cr_rope) == 24
-    assert ctypes.sizeof(B.cr_options) == 48
+    assert ctypes.sizeof(B.cr_options) == 72
+    assert ctypes.sizeof(B.cr_pipeline_item) == 56
     assert ctypes.sizeof(B.cr_kv_pages) == 24
     o = B.cr_options()
     B.load().cr_default_options(ctypes.byref(o))
     assert (o.mask, o.reinject, o.residual, o.apply, o.keep_first_chunk) == (0, 1, 1, 0, 0)
-    assert not o.global_rope and not o.position_offset and not o.pages
+    assert not o.global_rope and not o.position_offset and not o.pages and not o.kv_out
 
 
 def _call_repair_ex(w, options, layout=None, dims=None):
@@ -313,3 +314,41 @@ def test_valid_pages_pass_host_validation():
     B.cr_repair_ex(0x10000, lay, np.array([0, 0]), None, 0x20000, _dims(W0), 0x30000,
                    B.cr_prepared_bytes(_dims(W0), lay), 0x40000,
                    B.cr_workspace_bytes(_dims(W0), lay, 0), None, B.Options(pages=pg))
+
+
+# ------------------------------------------------- out of place, pipeline
+def test_out_of_place_validation():
+    lay = _layout(W0)
+    assert _call_repair_ex(W0, B.Options(kv_out=0x50000, layout_out=None)) in ("CR_ERR_NULL",)
+    other = _layout(W0)
+    other.head_dim = W0.target.head_dim // 2
+    assert _call_repair_ex(W0, B.Options(kv_out=0x50000, layout_out=other)) == "CR_ERR_LAYOUT"
+    assert _call_repair_ex(W0, B.Options(kv_out=0x50008, layout_out=_layout(W0))) == "CR_ERR_LAYOUT"
+    assert _call_repair_ex(W0, B.Options(kv_out=0x10000, layout_out=_layout(W0))) == "CR_ERR_LAYOUT"
+
+
+def _call_pipeline(w, items, same_stream=False, staging_bytes=None, max_tokens=None):
+    t = w.target
+    dims = _dims(w)
+    lay = _layout(w)
+    mt = w.n_tokens if max_tokens is None else max_tokens
+    sb = B.cr_pipeline_staging_bytes(dims, lay, mt) if staging_bytes is None else staging_bytes
+    with pytest.raises(B.CrError) as e:
+        B.cr_repair_pipelined(0x1234, items, dims, lay, 0x30000, B.cr_prepared_bytes(dims, lay),
+                              0x100000, sb, mt, 0x40000, B.cr_workspace_bytes(dims, lay, mt),
+                              None, 0x77 if not same_stream else 0x88, 0x88)
+    return e.value.name
+
+
+def test_pipeline_validation():
+    w = W0
+    item = dict(kv_host=0x1000, embeds_host=0x2000, chunk_offsets=[0, 20, 40], position_offset=0,
+                kv_out=0x900000, layout_out=_layout(w), pages_out=None)
+    assert _call_pipeline(w, [item], same_stream=True) == "CR_ERR_DIMS"
+    assert _call_pipeline(w, [dict(item, kv_host=0)]) == "CR_ERR_NULL"
+    assert _call_pipeline(w, [item], max_tokens=30) == "CR_ERR_WORKSPACE"    # item larger than a slot
+    assert _call_pipeline(w, [item], staging_bytes=1) == "CR_ERR_WORKSPACE"
+    bad = _layout(w)
+    bad.n_layers += 1
+    assert _call_pipeline(w, [dict(item, layout_out=bad)]) == "CR_ERR_LAYOUT"
+    assert _call_pipeline(w, [dict(item, chunk_offsets=[0, 30, 20])]) == "CR_ERR_OFFSETS"

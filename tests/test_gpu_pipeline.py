@@ -1,0 +1,210 @@
+"""Out-of-place repair and the pipelined host -> device -> repair path on the
+GPU.  Both write the same values as the in-place repair of the same request:
+the out-of-place epilogue stores the repaired coordinates into a second cache
+(and copies the coordinates the variant leaves alone), the pipeline copies
+each request from pinned host memory into a staging slot and repairs it into
+its destination while the next request is in flight."""
+import numpy as np
+import pytest
+
+import workloads as W
+from helpers import repairer_for, small_workload, to_device
+from test_gpu_paged import _gather, _pool
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = 7.5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35139_amd import binding
+    binding.load()
+
+
+def _case(dtype="bf16", lengths=((70, 0, 133), (5, 61), (40,))):
+    return small_workload(lengths, seed=5, dtype=dtype, L=2, H=2, dh=64, E=128, d_c=64,
+                          d_b=128, n_heads=2, d_seg=8, ffn_mult=4)
+
+
+VARIANTS = {
+    "method": {},
+    "repair_k_only": dict(apply="k"),
+    "placed_keep_first": dict(global_rope=dict(theta=1e6), keep_first_chunk=True),
+    "direct_prediction": dict(residual=False),
+}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_out_of_place_matches_in_place(dtype, variant):
+    import torch
+    from paper_2609_35139_amd import binding as B
+    w = _case(dtype)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    n_req = len(w.request_chunks) - 1
+    opts = dict(VARIANTS[variant])
+    if "global_rope" in opts:
+        opts["position_offset"] = list(range(3, 3 + 7 * n_req, 7))
+    emb = to_device(w, inp.token_embeds)
+    kv_a = to_device(w, inp.kv)
+    rep.repair(kv_a, w.chunk_offsets, w.request_chunks, emb, options=B.Options(**opts))
+    kv_in = to_device(w, inp.kv)
+    before = kv_in.clone()
+    out = torch.full_like(kv_in, SENTINEL)
+    rep.repair(kv_in, w.chunk_offsets, w.request_chunks, emb,
+               options=B.Options(kv_out=out.data_ptr(), layout_out=rep.layout(w.n_tokens),
+                                 **opts))
+    torch.cuda.synchronize()
+    assert torch.equal(out, kv_a)
+    assert torch.equal(kv_in, before)
+
+
+@pytest.mark.parametrize("direction", ["strided_to_paged", "paged_to_strided"])
+def test_out_of_place_paged(direction):
+    import torch
+    from paper_2609_35139_amd import binding as B
+    w = _case("bf16")
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    t = w.target
+    bs = 16
+    emb = to_device(w, inp.token_embeds)
+    kv_a = to_device(w, inp.kv)
+    rep.repair(kv_a, w.chunk_offsets, w.request_chunks, emb, options=B.Options(apply="v"))
+    ref = kv_a.float().cpu().numpy()
+    pool, table = _pool(w, inp.kv.astype(np.float32), bs, 3, 29)
+    lay_p, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, pool.shape[2], bs,
+                               B.CR_DTYPE_BF16)
+    pages = dict(block_size=bs, n_blocks=pool.shape[2], stride_block=sB, block_table=table)
+    if direction == "strided_to_paged":
+        kv_in = to_device(w, inp.kv)
+        before = kv_in.clone()
+        out = to_device(w, np.full_like(pool, SENTINEL))
+        rep.repair(kv_in, w.chunk_offsets, w.request_chunks, emb,
+                   options=B.Options(apply="v", kv_out=out.data_ptr(), layout_out=lay_p,
+                                     pages_out=pages))
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()
+        assert np.array_equal(_gather(got, table, w.n_tokens, bs), ref)
+        used = np.zeros(got.shape[:4], bool)
+        for tok in range(w.n_tokens):
+            used[:, :, table[tok // bs], tok % bs] = True
+        assert np.all(got[~used] == SENTINEL)
+        assert torch.equal(kv_in, before)
+    else:
+        kv_p = to_device(w, pool)
+        before = kv_p.clone()
+        out = torch.full_like(kv_a, SENTINEL)
+        rep.repair(kv_p, w.chunk_offsets, w.request_chunks, emb, layout=lay_p,
+                   options=B.Options(apply="v", pages=pages, kv_out=out.data_ptr(),
+                                     layout_out=rep.layout(w.n_tokens)))
+        torch.cuda.synchronize()
+        assert np.array_equal(out.float().cpu().numpy(), ref)
+        assert torch.equal(kv_p, before)
+
+
+def _requests(w, inp):
+    """Per-request (layer-major cache [L][2][n][H][dh], embeddings, offsets)."""
+    off, rc = w.chunk_offsets, w.request_chunks
+    out = []
+    for r in range(len(rc) - 1):
+        t0, t1 = off[rc[r]], off[rc[r + 1]]
+        local = [o - t0 for o in off[rc[r]:rc[r + 1] + 1]]
+        out.append((np.ascontiguousarray(inp.kv[:, :, t0:t1]),
+                    np.ascontiguousarray(inp.token_embeds[t0:t1]), local))
+    return out
+
+
+def _pinned(w, arr):
+    import torch
+    from paper_2609_35139_amd.repairer import TORCH_DTYPE, storage_dtype
+    return torch.from_numpy(arr).to(TORCH_DTYPE[storage_dtype(w.dtype)]).pin_memory()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("placed", [False, True], ids=["method", "global_placement"])
+def test_pipeline_matches_direct_repair(dtype, placed):
+    import torch
+    from paper_2609_35139_amd import binding as B
+    lengths = ((70, 0, 133), (5, 61), (40,), (1,), (64, 64, 64), (17, 3))
+    w = _case(dtype, lengths)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    reqs = _requests(w, inp)
+    opts = dict(global_rope=dict(theta=1e6)) if placed else {}
+    # direct single-request repairs, in place on device copies
+    refs = []
+    for r, (kv_r, emb_r, off_r) in enumerate(reqs):
+        kv_d = to_device(w, kv_r)
+        o = dict(opts, position_offset=[11 * r]) if placed else opts
+        rep.repair(kv_d, off_r, [0, len(off_r) - 1], to_device(w, emb_r),
+                   options=B.Options(**o) if o else None)
+        refs.append(kv_d)
+    torch.cuda.synchronize()
+    max_tokens = max(o[-1] for _, _, o in reqs)
+    copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
+    hosts = [(_pinned(w, kv_r), _pinned(w, emb_r)) for kv_r, emb_r, _ in reqs]
+    staging = workspace = None
+    for rnd in range(2):          # a second call on the same handle reuses the slots
+        outs = [torch.full_like(ref, SENTINEL + rnd) for ref in refs]
+        items = [dict(kv_host=hk, embeds_host=he, chunk_offsets=off_r, position_offset=11 * r,
+                      kv_out=outs[r], layout_out=rep.layout(off_r[-1]))
+                 for r, ((hk, he), (_, _, off_r)) in enumerate(zip(hosts, reqs))]
+        torch.cuda.synchronize()  # the fills above ran on the current stream
+        staging, workspace = rep.repair_pipelined(
+            items, max_tokens, copy_s, comp_s, options=B.Options(**opts) if opts else None,
+            staging=staging, workspace=workspace)
+        comp_s.synchronize()
+        copy_s.synchronize()
+        for r in range(len(reqs)):
+            assert torch.equal(outs[r], refs[r]), (rnd, r)
+
+
+def test_pipeline_into_paged_pool():
+    """Every request lands in its own blocks of one shared pool."""
+    import torch
+    from paper_2609_35139_amd import binding as B
+    lengths = ((33, 20), (16,), (50, 1, 9))
+    w = _case("bf16", lengths)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    t = w.target
+    reqs = _requests(w, inp)
+    bs = 16
+    nb = [-(-o[-1] // bs) for _, _, o in reqs]
+    n_blocks = sum(nb) + 2
+    perm = np.random.default_rng(31).permutation(n_blocks).astype(np.int32)
+    tables, s = [], 0
+    for k in nb:
+        tables.append(perm[s:s + k])
+        s += k
+    pool = torch.full((t.n_layers, 2, n_blocks, bs, t.n_kv_heads, t.head_dim), SENTINEL,
+                      dtype=torch.bfloat16, device="cuda")
+    lay_p, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, n_blocks, bs,
+                               B.CR_DTYPE_BF16)
+    items = []
+    for r, (kv_r, emb_r, off_r) in enumerate(reqs):
+        items.append(dict(kv_host=_pinned(w, kv_r), embeds_host=_pinned(w, emb_r),
+                          chunk_offsets=off_r, kv_out=pool, layout_out=lay_p,
+                          pages_out=dict(block_size=bs, n_blocks=n_blocks, stride_block=sB,
+                                         block_table=tables[r])))
+    copy_s, comp_s = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    rep.repair_pipelined(items, max(o[-1] for _, _, o in reqs), copy_s, comp_s)
+    comp_s.synchronize()
+    got = pool.float().cpu().numpy()
+    used = np.zeros(got.shape[:4], bool)
+    for r, (kv_r, emb_r, off_r) in enumerate(reqs):
+        kv_d = to_device(w, kv_r)
+        rep.repair(kv_d, off_r, [0, len(off_r) - 1], to_device(w, emb_r))
+        torch.cuda.synchronize()
+        n = off_r[-1]
+        assert np.array_equal(_gather(got, tables[r], n, bs), kv_d.float().cpu().numpy()), r
+        for tok in range(n):
+            used[:, :, tables[r][tok // bs], tok % bs] = True
+    assert np.all(got[~used] == SENTINEL)
