@@ -205,6 +205,8 @@ def main():
     ap.add_argument("--workload", default="qwen3b-8x512")
     ap.add_argument("--oracle-chunks", type=int, default=8,
                     help="chunks per request in the CPU oracle sample (0 = skip)")
+    ap.add_argument("--variants", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the method's variants on the same batch")
     ap.add_argument("--pipeline-requests", type=int, default=4,
                     help="requests in the pinned-host pipelined measurement (0 = skip)")
     ap.add_argument("--cold", action="store_true",
@@ -361,7 +363,7 @@ def main():
     }
     variants = {}
     vsteps = max(1, min(args.steps, 10))
-    for name, opt in variant_opts.items():
+    for name, opt in (variant_opts if args.variants else {}).items():
         for _ in range(2):
             rep.repair(kv, off, req, emb, workspace=ws, stream=stream, options=opt)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -372,33 +374,34 @@ def main():
         torch.cuda.synchronize()
         vms = a.elapsed_time(b) / vsteps
         variants[name] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
-    # paged cache: the same batch in a pool of 16-token blocks under a
-    # shuffled block table, repaired in place through the table
-    bs = 16
-    nbt = -(-w.n_tokens // bs)
-    table = np.random.default_rng(0).permutation(nbt).astype(np.int32)
-    pool = torch.empty((t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim), dtype=kv.dtype,
-                       device="cuda")
-    flat = kv.view(t.n_layers, 2, w.n_tokens, t.n_kv_heads, t.head_dim)
-    pad = nbt * bs - w.n_tokens
-    src = torch.nn.functional.pad(flat, (0, 0, 0, 0, 0, pad)) if pad else flat
-    pool[:, :, torch.from_numpy(table).long().cuda()] = src.reshape(
-        t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim)
-    plan, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, nbt, bs,
-                              B.CR_DTYPE_BF16 if w.dtype == "bf16" else B.CR_DTYPE_F32)
-    popt = B.Options(pages=dict(block_size=bs, n_blocks=nbt, stride_block=sB,
-                                block_table=table))
-    for _ in range(2):
-        rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for _ in range(vsteps):
-        rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
-    b.record(stream)
-    torch.cuda.synchronize()
-    vms = a.elapsed_time(b) / vsteps
-    variants["paged_16_token_blocks"] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
-    del pool
+    if args.variants:
+        # paged cache: the same batch in a pool of 16-token blocks under a
+        # shuffled block table, repaired in place through the table
+        bs = 16
+        nbt = -(-w.n_tokens // bs)
+        table = np.random.default_rng(0).permutation(nbt).astype(np.int32)
+        pool = torch.empty((t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim), dtype=kv.dtype,
+                           device="cuda")
+        flat = kv.view(t.n_layers, 2, w.n_tokens, t.n_kv_heads, t.head_dim)
+        pad = nbt * bs - w.n_tokens
+        src = torch.nn.functional.pad(flat, (0, 0, 0, 0, 0, pad)) if pad else flat
+        pool[:, :, torch.from_numpy(table).long().cuda()] = src.reshape(
+            t.n_layers, 2, nbt, bs, t.n_kv_heads, t.head_dim)
+        plan, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, nbt, bs,
+                                  B.CR_DTYPE_BF16 if w.dtype == "bf16" else B.CR_DTYPE_F32)
+        popt = B.Options(pages=dict(block_size=bs, n_blocks=nbt, stride_block=sB,
+                                    block_table=table))
+        for _ in range(2):
+            rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(vsteps):
+            rep.repair(pool, off, req, emb, workspace=ws, layout=plan, stream=stream, options=popt)
+        b.record(stream)
+        torch.cuda.synchronize()
+        vms = a.elapsed_time(b) / vsteps
+        variants["paged_16_token_blocks"] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
+        del pool
     print("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in
                                             variants.items()), file=sys.stderr, flush=True)
 

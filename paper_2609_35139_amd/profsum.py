@@ -85,15 +85,48 @@ def kernel_stats(stats_csv, bench_json, command):
     return "\n".join(out) + "\n"
 
 
-def _per_dispatch(path, counter):
-    """{kernel name: [value per dispatch]} for one counter of a --pmc pass."""
-    vals = {}
+def _dispatches(path, counter):
+    """[(dispatch id, kernel name, value)] in dispatch order for one counter
+    of a --pmc pass (values of one dispatch summed over its rows)."""
+    vals, names = {}, {}
     for r in csv.DictReader(open(path)):
         if r["Counter_Name"] != counter:
             continue
-        vals.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
-        vals[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
-    return {k: list(v.values()) for k, v in vals.items()}
+        d = int(r["Dispatch_Id"])
+        vals[d] = vals.get(d, 0.0) + float(r["Counter_Value"])
+        names[d] = r["Kernel_Name"]
+    return [(d, names[d], vals[d]) for d in sorted(vals)]
+
+
+def _per_dispatch(path, counter):
+    """{kernel name: [value per dispatch]} for one counter of a --pmc pass."""
+    out = {}
+    for _, name, v in _dispatches(path, counter):
+        out.setdefault(name, []).append(v)
+    return out
+
+
+def gemm_sequence(n_blocks):
+    """Classes of the bias-epilogue GEMMs of one repair, in launch order."""
+    return (["gemm_compress", "gemm_inject", "gemm_token", "gemm_fuse"] +
+            ["gemm_oproj", "gemm_ffn1", "gemm_ffn2"] * n_blocks)
+
+
+def _class_values(path, counter, cls, bench):
+    """Counter values of the dispatches of one kernel class.  The GEMMs with
+    a bias epilogue share one device function; they are told apart by their
+    position in the repair's fixed launch order (the profiled command runs
+    nothing else that launches them)."""
+    sub = CLASS_KERNEL[cls][0]
+    ds = [(n, v) for _, n, v in _dispatches(path, counter) if sub in n]
+    if sub != "EpiBias":
+        return [v for _, v in ds]
+    per_step = {k["class"]: k["launches_per_step"] for k in bench["kernels"]}
+    seq = gemm_sequence(per_step.get("gemm_oproj", 0))
+    if len(ds) % len(seq):
+        raise ValueError(f"{len(ds)} bias-epilogue GEMM dispatches do not split into "
+                         f"repairs of {len(seq)}")
+    return [v for i, (_, v) in enumerate(ds) if seq[i % len(seq)] == cls]
 
 
 def _calibration(per_kernel, copy_bytes):
@@ -119,7 +152,7 @@ def traffic(fetch_csv, write_csv, bench_json, cls, command):
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         per = _per_dispatch(path, counter)
         factor = _calibration(per, calib)
-        ks = [v for n, vs in per.items() if sub in n for v in vs]
+        ks = _class_values(path, counter, cls, b)
         if not ks:
             raise ValueError(f"no dispatch of {sub} in {path}")
         kib = sum(ks) / len(ks)
