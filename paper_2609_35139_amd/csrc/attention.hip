@@ -19,15 +19,22 @@
 // V arrives transposed (vt[head][d][token]) from the QKV epilogue, so the
 // A operand of O^T = V^T P^T is a contiguous 16-byte read.  K and V^T tiles
 // stream through a four-stage LDS ring filled by global_load_lds.  The
-// softmax reference max is only raised when a row max grows by more than
-// 2^8 (in exp2 units), which keeps probabilities <= 256 and skips almost
-// every rescale of the output accumulators.
+// softmax keeps a per-row reference max that is not a running max: the
+// score accumulators start at minus the reference, and the exact tile max is
+// taken (with a rescale of the output accumulators) only for a row's first
+// keys or when a tile's probability sum exceeds 2^24.  Softmax is invariant
+// to the reference, so this changes rounding only, and per score the VALU
+// does an exp2, half a pack and half a dot2 instead of also a max and a
+// subtraction.
 #include <climits>
 #include <type_traits>
 
 #include "launch.h"
 
 namespace cr {
+
+// largest tile row sum accepted without re-deriving the reference max
+constexpr float kMaxTileSum = 16777216.0f;   // 2^24
 
 template <typename T, int D, int STAGES_ = 4>
 struct AttnCfg {
@@ -161,7 +168,13 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   f32x16 oacc[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) oacc[d] = f32x16{};
+  // m_ref: the row's reference max (exp2 units), shared by both lane halves
+  // of a query; negm holds -m_ref (0 while there is none) as the score
+  // accumulators' initial value
   float m_ref = -INFINITY, lsum = 0.f;
+  f32x16 negm;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) negm[i] = 0.f;
 
   // group-local tile i (workgroup tile 2i + grp) into ring slot SLOT
   auto issue = [&](int i, int slot_bytes) {
@@ -197,12 +210,24 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
 #pragma unroll
       for (int kk = 0; kk < QF; ++kk)
         kf[rt][kk] = *reinterpret_cast<const frag*>(kp[kk] + (SO + rt * 32 * C::RBK));
+    // V^T fragments of this tile for O^T += V^T P^T, read before the score
+    // products so that their LDS latency hides behind the MFMAs and softmax
+    frag vf[2][PS][DT];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int s2 = 0; s2 < PS; ++s2)
+#pragma unroll
+        for (int d = 0; d < DT; ++d)
+          vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
+    // the accumulators start at -m_use, so the scores arrive already shifted
+    // by the row's reference max (no per-score subtraction)
     f32x16 s[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      s[rt] = f32x16{};
+      s[rt] = MM::mma(kf[rt][0], qf[0], negm);
 #pragma unroll
-      for (int kk = 0; kk < QF; ++kk) s[rt] = MM::mma(kf[rt][kk], qf[kk], s[rt]);
+      for (int kk = 1; kk < QF; ++kk) s[rt] = MM::mma(kf[rt][kk], qf[kk], s[rt]);
     }
     const int k0 = kb + (2 * it + grp) * C::BKV;
     if (!(k0 >= wmax_lo && k0 + C::BKV <= wmin_hi)) {
@@ -214,47 +239,58 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
           if (key < mlo || key >= mhi) s[rt][i] = -INFINITY;
         }
     }
-    float mx = -INFINITY;
+    // probabilities packed straight into the B operand of P V; the tile's
+    // row sum is taken over the packed values the product uses
+    frag pb[2][PS];
+    auto probs = [&](auto shifted, float shift) {
+      float ts = 0.f;
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+      for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rt][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-    // the reference max only moves when a row max exceeds it by 2^8 in
-    // exp2 units: probabilities stay <= 256 and rescales are rare
-    if (__any(mx > m_ref + 8.0f)) {
-      const float m_new = fmaxf(m_ref, mx);
+        for (int s2 = 0; s2 < PS; ++s2) {
+          float pv[KPL];
+#pragma unroll
+          for (int e = 0; e < KPL; ++e)
+            pv[e] = __builtin_amdgcn_exp2f(decltype(shifted)::value ? s[rt][s2 * KPL + e] - shift
+                                                                    : s[rt][s2 * KPL + e]);
+          pb[rt][s2] = pack_frag(pv, (frag*)nullptr);
+          ts = frag_sum(pb[rt][s2], ts);
+        }
+      return ts;
+    };
+    // Fast path: the reference max stays where it is.  A probability is at
+    // most its lane's tile sum, so a sum <= kMaxTileSum rules out overflow
+    // (O and l accumulate in fp32 with ample range).  Otherwise, and for a
+    // row without a reference yet, the wave takes the exact row max, rescales
+    // its accumulators and recomputes the tile's probabilities.
+    bool exact = __any(m_ref == -INFINITY);
+    float ts = 0.f;
+    if (!exact) {
+      ts = probs(std::false_type{}, 0.f);
+      exact = __any(!(ts <= kMaxTileSum));
+    }
+    if (exact) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rt][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
+      const float m_new = fmaxf(m_ref, mx + m_use);
       const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_ref - m_new);
-      m_ref = m_new;
       lsum *= alpha;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[d][i] *= alpha;
+      m_ref = m_new;
+      ts = probs(std::true_type{}, m_new == -INFINITY ? 0.f : m_new - m_use);
+      const float nm = m_new == -INFINITY ? 0.f : -m_new;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) negm[i] = nm;
     }
-    const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
-    // probabilities packed straight into the B operand of P V; the row sum
-    // is taken over the packed values the product uses
-    frag pb[2][PS];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int s2 = 0; s2 < PS; ++s2) {
-        float pv[KPL];
-#pragma unroll
-        for (int e = 0; e < KPL; ++e) pv[e] = __builtin_amdgcn_exp2f(s[rt][s2 * KPL + e] - m_use);
-        pb[rt][s2] = pack_frag(pv, (frag*)nullptr);
-        lsum = frag_sum(pb[rt][s2], lsum);
-      }
-    // O^T += V^T P^T; all fragment reads first
-    frag vf[2][PS][DT];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int s2 = 0; s2 < PS; ++s2)
-#pragma unroll
-        for (int d = 0; d < DT; ++d)
-          vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
+    lsum += ts;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll

@@ -457,6 +457,11 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
       dma16(bsrc[r] + kt * 128, base + G::BM * 128 + (r * G::NW + wave) * 1024);
   };
 
+  // the epilogue's global loads (bias, residuals, the stale cache) go out
+  // before the main loop and land while it runs
+  typename Epi::template Pre<G::BM, G::BN> pre;
+  epi.template prefetch<G::BM, G::BN>(pre, m0, n0, M, N);
+
   f32x16 acc[G::TM][G::TN];
 #pragma unroll
   for (int i = 0; i < G::TM; ++i)
@@ -500,8 +505,6 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
   // 4g .. 4g+3, the consecutive columns wn + j*32 + 8g + 4*(l >> 5) + [0, 4).
   // The epilogue's global loads go out first; the tile is then staged whole
   // with 16-byte LDS writes over the ring.
-  typename Epi::template Pre<G::BM, G::BN> pre;
-  epi.template prefetch<G::BM, G::BN>(pre, m0, n0, M, N);
   __syncthreads();  // ring no longer read
   float* Cs = reinterpret_cast<float*>(smem);
 #pragma unroll
