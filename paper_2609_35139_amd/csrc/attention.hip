@@ -212,14 +212,19 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
         kf[rt][kk] = *reinterpret_cast<const frag*>(kp[kk] + (SO + rt * 32 * C::RBK));
     // V^T fragments of this tile for O^T += V^T P^T, read before the score
     // products so that their LDS latency hides behind the MFMAs and softmax
+    // (bf16; the fp32 fragments are too many registers to hold that long)
+    constexpr bool kEarlyV = sizeof(T) == 2;
     frag vf[2][PS][DT];
+    auto read_v = [&] {
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+      for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-      for (int s2 = 0; s2 < PS; ++s2)
+        for (int s2 = 0; s2 < PS; ++s2)
 #pragma unroll
-        for (int d = 0; d < DT; ++d)
-          vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
+          for (int d = 0; d < DT; ++d)
+            vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
+    };
+    if constexpr (kEarlyV) read_v();
     // the accumulators start at -m_use, so the scores arrive already shifted
     // by the row's reference max (no per-score subtraction)
     f32x16 s[2];
@@ -291,6 +296,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
       for (int i = 0; i < 16; ++i) negm[i] = nm;
     }
     lsum += ts;
+    if constexpr (!kEarlyV) read_v();
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
