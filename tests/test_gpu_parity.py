@@ -61,6 +61,14 @@ SMALL = [
          n_heads=4, d_seg=24, n_blocks=3),
     dict(lengths=((1,), (2, 3), (64,)), dtype="f32", L=1, H=1, dh=32, E=64, d_c=64, d_b=128,
          n_heads=2, d_seg=32),
+    # largest supported target head (256) and head sizes that are odd
+    # multiples of 32 (segment projections of 3 and 7 MFMA k-steps)
+    dict(lengths=((65, 130), (3,)), dtype="bf16", L=1, H=2, dh=256, E=128, d_c=64, d_b=128,
+         n_heads=2, d_seg=16),
+    dict(lengths=((40, 97),), dtype="f32", L=2, H=3, dh=96, E=64, d_c=64, d_b=128,
+         n_heads=4, d_seg=8),
+    dict(lengths=((128, 1), (77,)), dtype="bf16", L=1, H=1, dh=224, E=64, d_c=128, d_b=128,
+         n_heads=2, d_seg=24),
 ]
 
 
@@ -72,6 +80,27 @@ def test_parity_small(cfg):
     inp = W.make_inputs(w)
     Y = gpu_repair(inp)
     assert_parity(Y, oracle_repair(inp), W.kv_layer_major_to_canonical(inp.kv), w)
+
+
+def test_empty_batch_is_a_no_op():
+    """Requests whose chunks are all empty: nothing is launched, the call
+    succeeds and the cache buffer is untouched."""
+    import torch
+    from paper_2609_35139_amd import binding as B
+    w = small_workload(((5,),), dtype="bf16", L=1, H=1, dh=64, E=64, d_c=64, d_b=128,
+                       n_heads=2, d_seg=8)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    kv = torch.full((64,), 3.0, dtype=torch.bfloat16, device="cuda")
+    emb = torch.zeros((1, w.target.d_model), dtype=torch.bfloat16, device="cuda")
+    ws = rep.workspace(0)
+    stream = torch.cuda.current_stream().cuda_stream
+    args = (kv.data_ptr(), rep.layout(0), [0, 0, 0], [0, 1, 2], emb.data_ptr(), rep.dims,
+            rep.prepared.data_ptr(), rep.prepared_bytes, ws.data_ptr(), ws.numel(), stream)
+    B.cr_repair(*args)
+    B.cr_repair_ex(*args, B.Options(global_rope=dict(theta=1e4), position_offset=[0, 0]))
+    torch.cuda.synchronize()
+    assert torch.all(kv == 3.0)
 
 
 @pytest.mark.parametrize("i", [0, 1])
