@@ -418,6 +418,27 @@ __device__ __forceinline__ void wait_slab(int ahead) {
   wait_vmcnt<0>();
 }
 
+// Tile of this workgroup.  Workgroups are dealt to the 8 XCDs round-robin
+// (linear id i runs on XCD i % 8), and each XCD has its own L2, so ids are
+// first regrouped so that each XCD receives a contiguous run of tiles, and
+// runs are walked in groups of TILE_GROUP tile rows, column by column: the
+// workgroups resident on one XCD share a few A row panels and B column
+// panels instead of each XCD fetching every panel.
+constexpr int TILE_GROUP = 8;
+template <typename G>
+__device__ __forceinline__ void tile_of(int M, int N, int& tm, int& tn) {
+  const int gm = (M + G::BM - 1) / G::BM, gn = (N + G::BN - 1) / G::BN;
+  const int total = gm * gn;
+  int id = blockIdx.x;
+  if (total % 8 == 0) id = (id % 8) * (total / 8) + id / 8;
+  const int per_group = TILE_GROUP * gn;
+  const int first = (id / per_group) * TILE_GROUP;
+  const int rows = min(gm - first, TILE_GROUP);
+  const int k = id % per_group;
+  tm = first + k % rows;
+  tn = k / rows;
+}
+
 template <typename T, typename G, typename Epi>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, int64_t lda,
                                                       const T* __restrict__ B, int64_t ldb,
@@ -427,7 +448,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
   __shared__ __align__(1024) char smem[G::LDS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.y * G::BM, n0 = blockIdx.x * G::BN;
+  int tm, tn;
+  tile_of<G>(M, N, tm, tn);
+  const int m0 = tm * G::BM, n0 = tn * G::BN;
   const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
 
   // DMA sources: in round r a wave fills 1 KB = rows (r*NW + wave)*8 + [0, 8)
@@ -525,7 +548,9 @@ template <typename T, typename G, typename Epi>
 static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N,
                                int K, const Epi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  dim3 grid((N + G::BN - 1) / G::BN, (M + G::BM - 1) / G::BM);
+  const int64_t tiles = (int64_t)((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM);
+  if (tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  dim3 grid((unsigned)tiles);
   CR_LAUNCH((gemm_nt_kernel<T, G, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K,
                      epi);
   return hipGetLastError();
