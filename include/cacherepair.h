@@ -10,11 +10,15 @@
  * where h^B is the output of B Repair Blocks over the fused stale features
  * and token embeddings (paper Section 4.1, "StaleEncoder and token fusion",
  * "Repair Blocks and stale-feature reinjection", "KV residual output and
- * global RoPE").  The add is done in place in the caller's cache.  cr_repair
- * leaves K canonical; cr_repair_ex can place the repaired keys at their
- * global positions in the same pass and runs the paper's controlled
- * variants (attention topologies, entrance-only features, direct prediction,
- * output choices).
+ * global RoPE").  cr_repair adds in place in the caller's cache and leaves K
+ * canonical; cr_repair_ex can place the repaired keys at their global
+ * positions in the same pass, runs the paper's controlled variants
+ * (attention topologies, entrance-only features, direct prediction, output
+ * choices), reads and writes paged caches through a block table and can
+ * write the result into a second cache (out of place).  cr_repair_pipelined
+ * overlaps the host-to-device copy of one request with the repair of the
+ * previous one.  cr_rotate_keys applies the target's rotary encoding (or its
+ * inverse) to a cache's keys.
  *
  * Conventions shared by every entry point:
  *  - Plain C: no C++ or torch types.  All sizes are element counts unless the
