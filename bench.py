@@ -402,8 +402,9 @@ def main():
         vms = a.elapsed_time(b) / vsteps
         variants["paged_16_token_blocks"] = {"ms_per_step": vms, "tokens_per_s": w.n_tokens / (vms * 1e-3)}
         del pool
-    print("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in
-                                            variants.items()), file=sys.stderr, flush=True)
+    if variants:
+        print("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in
+                                                variants.items()), file=sys.stderr, flush=True)
 
     pipeline = None
     if args.pipeline_requests > 0:
