@@ -205,6 +205,8 @@ def main():
     ap.add_argument("--workload", default="qwen3b-8x512")
     ap.add_argument("--oracle-chunks", type=int, default=8,
                     help="chunks per request in the CPU oracle sample (0 = skip)")
+    ap.add_argument("--graph", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the step captured in a HIP graph")
     ap.add_argument("--variants", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the method's variants on the same batch")
     ap.add_argument("--pipeline-requests", type=int, default=4,
@@ -267,6 +269,25 @@ def main():
     wall = time.perf_counter() - wall0
     ms = e0.elapsed_time(e1) / args.steps
     print(f"[bench] {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # ---- the same step captured once in a HIP graph and replayed K times
+    graph_ms = None
+    if args.graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            step()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        with torch.cuda.stream(stream):
+            for _ in range(args.steps):
+                g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = a.elapsed_time(b) / args.steps
+        del g
+        print(f"[bench] graph replay {graph_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     # ---- per-kernel HIP events recorded by the library on the same stream
     work = algorithmic_work(w)
@@ -450,6 +471,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "cold_ms_per_step": cold,
+        "graph_ms_per_step": graph_ms,
         "measured_peaks": measured,
         "variants": variants,
         "pipeline": pipeline,
