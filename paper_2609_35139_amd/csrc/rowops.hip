@@ -86,57 +86,96 @@ hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g,
 // ------------------------------------------------- StaleEncoder stage 1
 // u_g = (x_g / sigma_g) W1_g + b1_g for every segment g = (l, kv, h), with
 // 1/sigma folded into the prepared weights wseg[g][32][d_h] (rows >= d_seg
-// are zero).  One workgroup = 64 tokens of one segment, 16 tokens per wave,
-// 16x16 MFMA atoms fed straight from the cache rows: every lane issues all
-// of its loads (one 16-byte run of its token's head vector per k-step, plus
-// the segment's weights) before the first product.
-template <typename T, int DH>
+// are zero) and bseg[g][32].  One workgroup = TOK = 16*TB tokens x four
+// consecutive segments (one per wave), so a workgroup streams whole runs of
+// the cache rows and a wave's weight fragments serve TB token blocks.  The
+// product is formed transposed, U^T = W X^T, on 16x16 MFMA atoms fed
+// straight from the cache rows (every load is issued before the first
+// product): a lane ends with four consecutive output columns of one token.
+// The workgroup's outputs (4*d_seg contiguous columns per token) are staged
+// in LDS and written as 16-byte row runs.
+template <typename T, int DH, int TB>
 __global__ __launch_bounds__(256) void compress_segments_kernel(
     const T* __restrict__ kv, KvStrides ks, const T* __restrict__ wseg,
-    const float* __restrict__ bseg, T* __restrict__ U, int64_t ldu, int d_seg, int N, int Kc) {
+    const float* __restrict__ bseg, T* __restrict__ U, int64_t ldu, int d_seg, int N, int S,
+    int Kc) {
   using MM = Mma16<T>;
   using frag = typename MM::frag;
   constexpr int NK = DH / MM::KSTEP;
+  constexpr int TOK = 16 * TB;
+  constexpr int VE = 16 / (int)sizeof(T);
+  __shared__ __align__(16) T stage[TOK * 128];   // [token][4 segments x <= 32 columns]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int g = blockIdx.y;
-  const int h = g % ks.n_kv_heads, lk = g / ks.n_kv_heads;
-  const T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
-                  (int64_t)h * ks.head;
-  const int t0 = blockIdx.x * 64 + wave * 16;
-  const int tr = t0 + (lane & 15);
+  const int g0 = blockIdx.y * 4, g = g0 + wave;
+  const int span = min(4, S - g0) * d_seg;
+  const int t0 = blockIdx.x * TOK;
   const int fk = (lane >> 4) * MM::KPL;
-  const T* wg = wseg + (int64_t)g * 32 * DH;
-  frag a[NK], w[2][NK];
+  if (g < S) {
+    const int h = g % ks.n_kv_heads, lk = g / ks.n_kv_heads;
+    const T* base = kv + (int64_t)(lk >> 1) * ks.layer + (int64_t)(lk & 1) * ks.kv +
+                    (int64_t)h * ks.head;
+    const T* wg = wseg + (int64_t)g * 32 * DH;
+    frag x[TB][NK], w[2][NK];
 #pragma unroll
-  for (int k = 0; k < NK; ++k)
-    a[k] = tr < N ? load_frag<T, frag>(base + ks.tok(tr) + k * MM::KSTEP + fk) : frag{};
+    for (int b = 0; b < TB; ++b) {
+      const int t = t0 + b * 16 + (lane & 15);
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+      for (int k = 0; k < NK; ++k)
+        x[b][k] = t < N ? load_frag<T, frag>(base + ks.tok(t) + k * MM::KSTEP + fk) : frag{};
+    }
 #pragma unroll
-    for (int k = 0; k < NK; ++k)
-      w[j][k] = load_frag<T, frag>(wg + (j * 16 + (lane & 15)) * DH + k * MM::KSTEP + fk);
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-  for (int k = 0; k < NK; ++k)
+      for (int k = 0; k < NK; ++k)
+        w[j][k] = load_frag<T, frag>(wg + (j * 16 + (lane & 15)) * DH + k * MM::KSTEP + fk);
+    // output columns j*16 + (lane >> 4)*4 + e of token b*16 + (lane & 15)
+    float bb[2][4];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[j] = MM::mma(a[k], w[j][k], acc[j]);
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = j * 16 + (lane & 15);
-    if (col < d_seg) {
-      const float bb = bseg[g * 32 + col];
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int t = t0 + (lane >> 4) * 4 + e;
-        if (t < N) U[(int64_t)t * ldu + g * d_seg + col] = from_f32<T>(acc[j][e] + bb);
+        const int c = j * 16 + (lane >> 4) * 4 + e;
+        bb[j][e] = c < d_seg ? bseg[g * 32 + c] : 0.f;
       }
+#pragma unroll
+    for (int b = 0; b < TB; ++b) {
+      f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int k = 0; k < NK; ++k)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[j] = MM::mma(w[j][k], x[b][k], acc[j]);
+      const int r = b * 16 + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int c = j * 16 + (lane >> 4) * 4 + e;
+          if (c < d_seg) stage[r * 128 + wave * d_seg + c] = from_f32<T>(acc[j][e] + bb[j][e]);
+        }
     }
   }
-  if (g == 0) {  // zero the K padding of U for this wave's tokens
-    for (int idx = lane; idx < 16 * (ldu - Kc); idx += 64) {
-      const int t = t0 + idx / (int)(ldu - Kc);
-      const int c = Kc + idx % (int)(ldu - Kc);
-      if (t < N) U[(int64_t)t * ldu + c] = from_f32<T>(0.f);
+  __syncthreads();
+  // token rows of `span` contiguous columns from column g0*d_seg
+  const int64_t col0 = (int64_t)g0 * d_seg;
+  if (span % VE == 0 && col0 % VE == 0) {
+    const int cpr = span / VE;
+    for (int i = threadIdx.x; i < TOK * cpr; i += 256) {
+      const int r = i / cpr, c = (i % cpr) * VE, t = t0 + r;
+      if (t < N)
+        *reinterpret_cast<uint4*>(U + (int64_t)t * ldu + col0 + c) =
+            *reinterpret_cast<const uint4*>(stage + r * 128 + c);
+    }
+  } else {
+    for (int i = threadIdx.x; i < TOK * span; i += 256) {
+      const int r = i / span, c = i % span, t = t0 + r;
+      if (t < N) U[(int64_t)t * ldu + col0 + c] = stage[r * 128 + c];
+    }
+  }
+  if (blockIdx.y == 0) {  // zero the K padding of U for these tokens
+    const int pad = (int)(ldu - Kc);
+    for (int idx = threadIdx.x; idx < TOK * pad; idx += 256) {
+      const int t = t0 + idx / pad;
+      if (t < N) U[(int64_t)t * ldu + Kc + idx % pad] = from_f32<T>(0.f);
     }
   }
 }
@@ -147,11 +186,16 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
                              hipStream_t s) {
   if (N <= 0) return hipSuccess;
   const int S = 2 * n_layers * ks.n_kv_heads;
-  dim3 grid((N + 63) / 64, S);
+  // four 16-token blocks per wave (bf16) once the grid still fills the chip
+  // several times over; one block otherwise and for fp32 (register budget)
+  const bool wide = sizeof(T) == 2 && (int64_t)((N + 63) / 64) * ((S + 3) / 4) >= 1024;
+#define CR_COMPRESS_TB(DH, TB)                                                                 \
+  CR_LAUNCH((compress_segments_kernel<T, DH, TB>), dim3((N + 16 * TB - 1) / (16 * TB), (S + 3) / 4), \
+            dim3(256), 0, s, kv, ks, wseg, bseg, U, ldu, d_seg, N, S, S * d_seg)
 #define CR_COMPRESS(DH)                                                                        \
   case DH:                                                                                     \
-    CR_LAUNCH((compress_segments_kernel<T, DH>), grid, dim3(256), 0, s, kv, ks, wseg, \
-                       bseg, U, ldu, d_seg, N, S * d_seg);                                     \
+    if (wide) CR_COMPRESS_TB(DH, (sizeof(T) == 2 ? 4 : 1));                                    \
+    else CR_COMPRESS_TB(DH, 1);                                                                \
     break;
   switch (ks.head_dim) {
     CR_COMPRESS(32) CR_COMPRESS(64) CR_COMPRESS(96) CR_COMPRESS(128)
@@ -159,6 +203,7 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
     default: return hipErrorInvalidValue;
   }
 #undef CR_COMPRESS
+#undef CR_COMPRESS_TB
   return hipGetLastError();
 }
 
