@@ -558,12 +558,13 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
 
 // 128x128 tiles.  Grids of more than one workgroup per CU use a two-slab
 // ring (64 KB, two workgroups resident per CU hide each other's latency);
-// grids that fit in one pass over the 256 CUs use a three-slab ring instead.
+// grids that fit in one pass over the 256 CUs use a four-slab ring instead
+// (one workgroup per CU: three slabs in flight cover the fetch latency).
 template <typename T, typename Epi>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                          const Epi& epi, hipStream_t s) {
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
-  if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 2, 3>>(A, lda, B, ldb, M, N, K, epi, s);
+  if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   return launch_tiled<T, GemmTile<T, 2, 2, 2>>(A, lda, B, ldb, M, N, K, epi, s);
 }
 

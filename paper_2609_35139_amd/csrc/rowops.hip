@@ -19,57 +19,65 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
 // ------------------------------------------------------------- LayerNorm
 // y = (x - mean) / sqrt(var + eps) * g + b over rows of C elements, biased
 // variance, statistics in fp32 from values held in registers (two passes).
-template <typename T>
+// A wave normalises R rows with one copy of gamma and beta in registers;
+// every load (R rows, gamma, beta) is issued before the first reduction.
+template <typename T, int MAXV, int R>
 __global__ __launch_bounds__(256) void layernorm_kernel(const T* __restrict__ x, int64_t ldx,
                                                         T* __restrict__ y, int64_t ldy,
                                                         const float* __restrict__ g,
                                                         const float* __restrict__ b, int M,
                                                         int C, float eps) {
-  constexpr int MAXV = 4;  // 4 x 8 values per lane: C <= 2048
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;
-  const T* xr = x + (int64_t)row * ldx;
-  // every load (row, gamma, beta) is issued before the first reduction
-  float v[MAXV][8], gv[MAXV][8], bv[MAXV][8];
+  const int row0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
+  if (row0 >= M) return;
+  float v[R][MAXV][8], gv[MAXV][8], bv[MAXV][8];
 #pragma unroll
   for (int k = 0; k < MAXV; ++k) {
     const int c = (k * 64 + lane) * 8;
     if (c < C) {
-      Vec8<T> t; t.load(xr + c); t.to_float(v[k]);
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (row0 + r < M) { Vec8<T> t; t.load(x + (int64_t)(row0 + r) * ldx + c); t.to_float(v[r][k]); }
       load8(g + c, gv[k]);
       load8(b + c, bv[k]);
     }
   }
-  float sum = 0.f;
+  float mean[R], rstd[R];
 #pragma unroll
-  for (int k = 0; k < MAXV; ++k) {
-    const int c = (k * 64 + lane) * 8;
-    if (c < C) {
+  for (int r = 0; r < R; ++r) {
+    float sum = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sum += v[k][e];
-    }
+    for (int k = 0; k < MAXV; ++k)
+      if ((k * 64 + lane) * 8 < C) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += v[r][k][e];
+      }
+    mean[r] = wave_sum(sum) / (float)C;
   }
-  const float mean = wave_sum(sum) / (float)C;
-  float sq = 0.f;
 #pragma unroll
-  for (int k = 0; k < MAXV; ++k) {
-    const int c = (k * 64 + lane) * 8;
-    if (c < C) {
+  for (int r = 0; r < R; ++r) {
+    float sq = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) { const float d = v[k][e] - mean; sq += d * d; }
-    }
+    for (int k = 0; k < MAXV; ++k)
+      if ((k * 64 + lane) * 8 < C) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { const float d = v[r][k][e] - mean[r]; sq += d * d; }
+      }
+    rstd[r] = 1.0f / sqrtf(wave_sum(sq) / (float)C + eps);
   }
-  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)C + eps);
-  T* yr = y + (int64_t)row * ldy;
 #pragma unroll
-  for (int k = 0; k < MAXV; ++k) {
-    const int c = (k * 64 + lane) * 8;
-    if (c < C) {
-      float o[8];
+  for (int r = 0; r < R; ++r) {
+    if (row0 + r >= M) break;
+    T* yr = y + (int64_t)(row0 + r) * ldy;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (v[k][e] - mean) * rstd * gv[k][e] + bv[k][e];
-      Vec8<T> t; t.from_float(o); t.store(yr + c);
+    for (int k = 0; k < MAXV; ++k) {
+      const int c = (k * 64 + lane) * 8;
+      if (c < C) {
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (v[r][k][e] - mean[r]) * rstd[r] * gv[k][e] + bv[k][e];
+        Vec8<T> t; t.from_float(o); t.store(yr + c);
+      }
     }
   }
 }
@@ -78,8 +86,15 @@ template <typename T>
 hipError_t layernorm(const T* x, int64_t ldx, T* y, int64_t ldy, const float* g, const float* b,
                      int M, int C, float eps, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  CR_LAUNCH((layernorm_kernel<T>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
-                     g, b, M, C, eps);
+  // one row per wave: four resident workgroups per SIMD hide the reductions'
+  // latency (several rows per wave with fewer waves measured slower)
+  if (C <= 1024) {
+    CR_LAUNCH((layernorm_kernel<T, 2, 1>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
+              g, b, M, C, eps);
+  } else {
+    CR_LAUNCH((layernorm_kernel<T, 4, 1>), dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, y, ldy,
+              g, b, M, C, eps);
+  }
   return hipGetLastError();
 }
 
