@@ -1,8 +1,9 @@
 // Tiled MFMA GEMM for the repair network's dense projections (gfx950).
 //
 // C[M][N] = A[M][K] * B[N][K]^T with both operands K-contiguous (activations
-// row-major, weights prepared as [out][in]).  A 256-thread workgroup owns an
-// output tile split in four wave quadrants computed with 32x32 MFMA atoms.
+// row-major, weights prepared as [out][in]).  A workgroup owns an output
+// tile (128x128 on four waves or 256x256 on eight) split in wave sub-tiles
+// computed with 32x32 MFMA atoms.
 // K advances in slabs of 128 bytes per row, fetched straight from global
 // memory into an LDS ring with global_load_lds (no register staging); rows
 // are XOR-swizzled in LDS so fragment reads are conflict-free.  The MFMA
@@ -17,17 +18,18 @@
 
 namespace cr {
 
-// Tile geometry: a 2x2 grid of waves, each owning TM x TN MFMA atoms of
-// 32x32 (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32), so
-// the workgroup tile is (64*TM) x (64*TN).  K advances in slabs of one
-// 128-byte row per tile row; STAGES slabs live in the LDS ring, which the
-// staged output tile reuses.
-template <typename T, int TM_, int TN_, int STAGES_>
+// Tile geometry: a WGM x WGN grid of waves, each owning TM x TN MFMA atoms
+// of 32x32 (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32),
+// so the workgroup tile is (WGM*32*TM) x (WGN*32*TN).  K advances in slabs
+// of one 128-byte row per tile row; STAGES slabs live in the LDS ring.  The
+// fp32 output tile is staged through LDS over the ring, EPI_ROWS rows at a
+// time (the whole tile, or half of it for 256-row tiles).
+template <typename T, int TM_, int TN_, int STAGES_, int WGM_ = 2, int WGN_ = 2>
 struct GemmTile {
-  static constexpr int TM = TM_, TN = TN_, STAGES = STAGES_;
-  static constexpr int NW = 4, NT = 256;
+  static constexpr int TM = TM_, TN = TN_, STAGES = STAGES_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NW = WGM * WGN, NT = 64 * NW;
   static constexpr int WM = 32 * TM, WN = 32 * TN;
-  static constexpr int BM = 2 * WM, BN = 2 * WN;
+  static constexpr int BM = WGM * WM, BN = WGN * WN;
   static constexpr int BK = 128 / (int)sizeof(T);   // elements per 128-byte row
   static constexpr int VEC = 16 / (int)sizeof(T);   // elements per 16-byte chunk
   static constexpr int A_ROUNDS = BM * 8 / NT;      // 16-byte DMA ops per thread per slab
@@ -35,10 +37,13 @@ struct GemmTile {
   static constexpr int OPS = A_ROUNDS + B_ROUNDS;
   static constexpr int STAGE_BYTES = (BM + BN) * 128;
   static constexpr int LDC = BN + 4;                // fp32 staging row (16-byte aligned rows)
+  static constexpr int EPI_ROWS = BM > 128 ? BM / 2 : BM;
   static constexpr size_t LDS_MAIN = (size_t)STAGES * STAGE_BYTES;
-  static constexpr size_t LDS_C = (size_t)BM * LDC * sizeof(float);
+  static constexpr size_t LDS_C = (size_t)EPI_ROWS * LDC * sizeof(float);
   static constexpr size_t LDS = LDS_MAIN > LDS_C ? LDS_MAIN : LDS_C;
   static_assert(OPS * (STAGES - 2) <= 63, "vmcnt range");
+  static_assert(A_ROUNDS * NT == BM * 8 && B_ROUNDS * NT == BN * 8, "DMA rounds");
+  static_assert(WM % EPI_ROWS == 0 || EPI_ROWS % WM == 0, "staging passes");
 };
 
 // Epilogues see the staged tile Cs[ROWS][LDC] (fp32) whose element (r, c)
@@ -46,12 +51,12 @@ struct GemmTile {
 // strided set of rows, so per-column vectors (bias, sigma) are loaded once.
 // An epilogue has two phases: prefetch() issues its global loads into a
 // Pre record before the tile is staged, run() consumes the staged tile.
-template <int ROWS, int COLS>
+template <int ROWS, int COLS, int NT>
 struct SegMap {
   static constexpr int SEG = COLS / 8;            // segments per row
-  static constexpr int RSTEP = 256 / SEG;         // rows between a thread's passes
+  static constexpr int RSTEP = NT / SEG;          // rows between a thread's passes
   static constexpr int PASSES = ROWS / RSTEP;
-  static_assert(256 % SEG == 0 && ROWS % RSTEP == 0, "segment map");
+  static_assert(NT % SEG == 0 && ROWS % RSTEP == 0, "segment map");
   __device__ static int col() { return (threadIdx.x % SEG) * 8; }
   __device__ static int row(int p) { return threadIdx.x / SEG + p * RSTEP; }
 };
@@ -63,16 +68,17 @@ __device__ __forceinline__ void load8f(const float* p, float* v) {
 
 template <typename T>
 struct EpiBias {
+  static constexpr bool kWide = true;
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
   int64_t ldr2; int gelu;
-  template <int ROWS, int COLS>
+  template <int ROWS, int COLS, int NT>
   struct Pre {
     float b[8];
-    Vec8<T> rv[SegMap<ROWS, COLS>::PASSES], rv2[SegMap<ROWS, COLS>::PASSES];
+    Vec8<T> rv[SegMap<ROWS, COLS, NT>::PASSES], rv2[SegMap<ROWS, COLS, NT>::PASSES];
   };
-  template <int ROWS, int COLS>
-  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
-    using S = SegMap<ROWS, COLS>;
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS, NT>;
     const int gn = n0 + S::col();
     if (gn >= N) return;
     load8f(bias + gn, p.b);
@@ -84,10 +90,10 @@ struct EpiBias {
       if (resid2) p.rv2[q].load(resid2 + (int64_t)gm * ldr2 + gn);
     }
   }
-  template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, const Pre<ROWS, COLS>& p, int m0, int n0, int M,
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& p, int m0, int n0, int M,
                       int N) const {
-    using S = SegMap<ROWS, COLS>;
+    using S = SegMap<ROWS, COLS, NT>;
     const int c = S::col(), gn = n0 + c;
     if (gn >= N) return;
 #pragma unroll
@@ -118,14 +124,15 @@ struct EpiBias {
 
 template <typename T>
 struct EpiQKV {
+  static constexpr bool kWide = false;   // head-aligned Q/K/V split of 128-column tiles
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
-  template <int ROWS, int COLS>
-  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS>::PASSES]; };
-  template <int ROWS, int COLS>
-  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+  template <int ROWS, int COLS, int NT>
+  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS, NT>::PASSES]; };
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
     if (n0 >= 2 * d_b) return;      // V tiles load their bias per column in run()
-    using S = SegMap<ROWS, COLS>;
+    using S = SegMap<ROWS, COLS, NT>;
     const int half = d_head / 2;
     const int c = S::col(), hc = c % d_head;
     const int pc = hc < half ? c + half : c - half;
@@ -137,8 +144,8 @@ struct EpiQKV {
       p.pp[q] = gm < M ? pos[gm] : 0;
     }
   }
-  template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, const Pre<ROWS, COLS>& p, int m0, int n0, int M,
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& p, int m0, int n0, int M,
                       int N) const {
     if (n0 < 2 * d_b) {
       // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
@@ -146,7 +153,7 @@ struct EpiQKV {
       // Q leaves scaled by log2(e)/sqrt(d_head) (the attention works in exp2
       // units); K rows in [M, n_pad) get finite values from clamped rows
       // (padding read by the attention's last key tile).
-      using S = SegMap<ROWS, COLS>;
+      using S = SegMap<ROWS, COLS, NT>;
       const bool is_q = n0 < d_b;
       T* dst = is_q ? q : k;
       const int rows_out = is_q ? M : (int)n_pad;
@@ -195,7 +202,7 @@ struct EpiQKV {
       // reads of the staged tile are conflict-free.  Rows in [M, n_pad) hold
       // values computed from clamped rows: finite padding.
       constexpr int RSEG = ROWS / 8;
-      for (int idx = threadIdx.x; idx < COLS * RSEG; idx += 256) {
+      for (int idx = threadIdx.x; idx < COLS * RSEG; idx += NT) {
         const int c = idx % COLS, r = (idx / COLS) * 8;
         const int gn = n0 + c, gm = m0 + r;
         if (gn >= N || gm + 8 > n_pad) continue;
@@ -225,13 +232,16 @@ __device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* 
 
 template <typename T>
 struct EpiExpand {
+  // 128x128 tiles: the stale-cache loads are issued before the main loop
+  // (measured faster than 256x256 tiles, whose loads wait for the loop's end)
+  static constexpr bool kWide = false;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
-  template <int ROWS, int COLS>
+  template <int ROWS, int COLS, int NT>
   struct Pre {
     float b[8], sg[8];
-    Vec8<T> x[SegMap<ROWS, COLS>::PASSES];
-    int kp[SegMap<ROWS, COLS>::PASSES];
+    Vec8<T> x[SegMap<ROWS, COLS, NT>::PASSES];
+    int kp[SegMap<ROWS, COLS, NT>::PASSES];
   };
   // 8 | d_h keeps a segment in one head
   __device__ bool selected(int gn, T** base) const {
@@ -239,9 +249,9 @@ struct EpiExpand {
     *base = kv_coord(kv, ks, gn, &is_k);
     return mode & (is_k ? EXPAND_K : EXPAND_V);
   }
-  template <int ROWS, int COLS>
-  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
-    using S = SegMap<ROWS, COLS>;
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS, NT>;
     const int gn = n0 + S::col();
     if (gn >= N) return;
     T* base;
@@ -259,9 +269,9 @@ struct EpiExpand {
       if (gm < M && need_x) p.x[q].load(base + ks.tok(gm));
     }
   }
-  template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
-    using S = SegMap<ROWS, COLS>;
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
+    using S = SegMap<ROWS, COLS, NT>;
     const int c = S::col(), gn = n0 + c;
     if (gn >= N) return;
     T* base;
@@ -299,25 +309,26 @@ struct EpiExpand {
 // straddles two 128-column tiles).
 template <typename T>
 struct EpiExpandRope {
+  static constexpr bool kWide = false;   // pair registers do not fit beside a 256x256 tile
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
   const float2* rope;      // [M][head_dim/2] scaled (cos, sin)
-  template <int COLS> struct Map {
+  template <int COLS, int NT> struct Map {
     static constexpr int PAIRS = COLS / 16;        // 8-pair groups per tile row
-    static constexpr int RSTEP = 256 / PAIRS;
+    static constexpr int RSTEP = NT / PAIRS;
   };
-  template <int ROWS, int COLS>
+  template <int ROWS, int COLS, int NT>
   struct Pre {
-    static constexpr int P = ROWS / Map<COLS>::RSTEP;
+    static constexpr int P = ROWS / Map<COLS, NT>::RSTEP;
     float b1[8], b2[8], s1[8], s2[8];
     Vec8<T> x1[P], x2[P];
     int kp[P];
   };
   struct Cols { int c1, c2, i0; bool is_k, on; T* b1; T* o1; };
-  template <int COLS>
+  template <int COLS, int NT>
   __device__ bool cols(int n0, int N, Cols& k) const {
     const int dh = ks.head_dim, half = dh / 2, sph = half / 8;
-    const int p = threadIdx.x % Map<COLS>::PAIRS;
+    const int p = threadIdx.x % Map<COLS, NT>::PAIRS;
     k.c1 = (p / sph) * dh + (p % sph) * 8;
     k.c2 = k.c1 + half;
     if (n0 + k.c2 >= N) return false;
@@ -328,16 +339,16 @@ struct EpiExpandRope {
     k.on = mode & (k.is_k ? EXPAND_K : EXPAND_V);
     return k.on || k.is_k || kvo;                  // stale V in place: nothing to write
   }
-  template <int ROWS, int COLS>
-  __device__ void prefetch(Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
     Cols k;
-    if (!cols<COLS>(n0, N, k)) return;
+    if (!cols<COLS, NT>(n0, N, k)) return;
     const int half = ks.head_dim / 2;
     load8f(bias + n0 + k.c1, p.b1); load8f(bias + n0 + k.c2, p.b2);
     load8f(sigma + n0 + k.c1, p.s1); load8f(sigma + n0 + k.c2, p.s2);
 #pragma unroll
-    for (int q = 0; q < Pre<ROWS, COLS>::P; ++q) {
-      const int gm = m0 + threadIdx.x / Map<COLS>::PAIRS + q * Map<COLS>::RSTEP;
+    for (int q = 0; q < Pre<ROWS, COLS, NT>::P; ++q) {
+      const int gm = m0 + threadIdx.x / Map<COLS, NT>::PAIRS + q * Map<COLS, NT>::RSTEP;
       p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
       if (gm < M) {
         const int64_t to = ks.tok(gm);
@@ -346,12 +357,12 @@ struct EpiExpandRope {
       }
     }
   }
-  template <int ROWS, int COLS, int LDC>
-  __device__ void run(const float* Cs, Pre<ROWS, COLS>& p, int m0, int n0, int M, int N) const {
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
     Cols k;
-    if (!cols<COLS>(n0, N, k)) return;
+    if (!cols<COLS, NT>(n0, N, k)) return;
     const int half = ks.head_dim / 2;
-    constexpr int P = Pre<ROWS, COLS>::P;
+    constexpr int P = Pre<ROWS, COLS, NT>::P;
     const bool res = mode & EXPAND_RESIDUAL;
     constexpr int GRP = P >= 2 ? 2 : P;             // passes whose (cos, sin) load together
 #pragma unroll
@@ -361,7 +372,7 @@ struct EpiExpandRope {
 #pragma unroll
       for (int u = 0; u < GRP; ++u) {
         const int gm =
-            min(m0 + (int)threadIdx.x / Map<COLS>::PAIRS + (q0 + u) * Map<COLS>::RSTEP, M - 1);
+            min(m0 + (int)threadIdx.x / Map<COLS, NT>::PAIRS + (q0 + u) * Map<COLS, NT>::RSTEP, M - 1);
         const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)gm * half + k.i0);
 #pragma unroll
         for (int e = 0; e < 4; ++e) cs[u][e] = t4[e];
@@ -370,7 +381,7 @@ struct EpiExpandRope {
 #pragma unroll
     for (int u = 0; u < GRP; ++u) {
       const int q = q0 + u;
-      const int r = threadIdx.x / Map<COLS>::PAIRS + q * Map<COLS>::RSTEP, gm = m0 + r;
+      const int r = threadIdx.x / Map<COLS, NT>::PAIRS + q * Map<COLS, NT>::RSTEP, gm = m0 + r;
       if (gm >= M) continue;
       float y1[8], y2[8];
       p.x1[q].to_float(y1);
@@ -440,7 +451,7 @@ __device__ __forceinline__ void tile_of(int M, int N, int& tm, int& tn) {
 }
 
 template <typename T, typename G, typename Epi>
-__global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, int64_t lda,
+__global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A, int64_t lda,
                                                       const T* __restrict__ B, int64_t ldb,
                                                       int M, int N, int K, Epi epi) {
   using MM = Mma32<T>;
@@ -451,7 +462,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
   int tm, tn;
   tile_of<G>(M, N, tm, tn);
   const int m0 = tm * G::BM, n0 = tn * G::BN;
-  const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
+  const int wm = (wave / G::WGN) * G::WM, wn = (wave % G::WGN) * G::WN;
 
   // DMA sources: in round r a wave fills 1 KB = rows (r*NW + wave)*8 + [0, 8)
   // of the tile; lane l reads the chunk that lands in slot (l & 7) of its row.
@@ -482,8 +493,12 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
 
   // the epilogue's global loads (bias, residuals, the stale cache) go out
   // before the main loop and land while it runs
-  typename Epi::template Pre<G::BM, G::BN> pre;
-  epi.template prefetch<G::BM, G::BN>(pre, m0, n0, M, N);
+  // (one staging pass: before the main loop, where they land while it runs;
+  // two passes: before each pass, so the loop keeps its registers)
+  constexpr int ER = G::EPI_ROWS;
+  constexpr bool kEarly = ER == G::BM;
+  typename Epi::template Pre<ER, G::BN, G::NT> pre;
+  if constexpr (kEarly) epi.template prefetch<ER, G::BN, G::NT>(pre, m0, n0, M, N);
 
   f32x16 acc[G::TM][G::TN];
 #pragma unroll
@@ -526,22 +541,29 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(const T* __restrict__ A, i
   // Epilogue.  With the weight tile as the MFMA's first operand, lane l of
   // atom (i, j) holds output row wm + i*32 + (l & 31) and, in registers
   // 4g .. 4g+3, the consecutive columns wn + j*32 + 8g + 4*(l >> 5) + [0, 4).
-  // The epilogue's global loads go out first; the tile is then staged whole
-  // with 16-byte LDS writes over the ring.
-  __syncthreads();  // ring no longer read
+  // The tile is staged EPI_ROWS rows at a time with 16-byte LDS writes over
+  // the ring, each pass after its epilogue loads have been issued.
   float* Cs = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int i = 0; i < G::TM; ++i)
+  for (int part = 0; part < G::BM / ER; ++part) {
+    if constexpr (!kEarly) epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
+    __syncthreads();  // ring (or the previous pass's rows) no longer read
 #pragma unroll
-    for (int j = 0; j < G::TN; ++j)
+    for (int i = 0; i < G::TM; ++i) {
+      const int r0 = wm + i * 32 - part * ER;   // first row of atom row i in this pass
+      if (r0 < 0 || r0 >= ER) continue;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        *reinterpret_cast<float4*>(Cs + (wm + i * 32 + fr) * G::LDC + wn + j * 32 + g * 8 +
-                                   (lane >> 5) * 4) =
-            make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                        acc[i][j][4 * g + 3]);
-  __syncthreads();
-  epi.template run<G::BM, G::BN, G::LDC>(Cs, pre, m0, n0, M, N);
+      for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<float4*>(Cs + (r0 + fr) * G::LDC + wn + j * 32 + g * 8 +
+                                     (lane >> 5) * 4) =
+              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                          acc[i][j][4 * g + 3]);
+    }
+    __syncthreads();
+    epi.template run<ER, G::BN, G::LDC, G::NT>(Cs, pre, m0 + part * ER, n0, M, N);
+  }
 }
 
 template <typename T, typename G, typename Epi>
@@ -551,18 +573,29 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
   const int64_t tiles = (int64_t)((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM);
   if (tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   dim3 grid((unsigned)tiles);
-  CR_LAUNCH((gemm_nt_kernel<T, G, Epi>), grid, dim3(256), 0, s, A, lda, B, ldb, M, N, K,
+  CR_LAUNCH((gemm_nt_kernel<T, G, Epi>), grid, dim3(G::NT), 0, s, A, lda, B, ldb, M, N, K,
                      epi);
   return hipGetLastError();
 }
 
-// 128x128 tiles.  Grids of more than one workgroup per CU use a two-slab
-// ring (64 KB, two workgroups resident per CU hide each other's latency);
-// grids that fit in one pass over the 256 CUs use a four-slab ring instead
-// (one workgroup per CU: three slabs in flight cover the fetch latency).
+// Tile choice.  bf16 products whose 256x256 tiling still fills the 256 CUs
+// take 256x256 tiles of eight waves (128x64 each, two per SIMD): half the
+// operand bytes per FLOP of a 128x128 tile, and one workgroup per CU with a
+// two-slab ring of 64 KB slabs.  Otherwise 128x128 tiles of four waves:
+// grids of more than one workgroup per CU use a two-slab ring (64 KB, two
+// workgroups resident per CU hide each other's latency); grids that fit in
+// one pass over the 256 CUs use a four-slab ring instead (one workgroup per
+// CU: three slabs in flight cover the fetch latency).  Epi::kWide is false
+// for epilogues that need a 128-column tile or more registers than the
+// 256x256 tile leaves.
 template <typename T, typename Epi>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                          const Epi& epi, hipStream_t s) {
+  if constexpr (sizeof(T) == 2 && Epi::kWide) {
+    const int64_t wide_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+    if (wide_tiles >= 256)
+      return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
+  }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
   if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   return launch_tiled<T, GemmTile<T, 2, 2, 2>>(A, lda, B, ldb, M, N, K, epi, s);
@@ -582,7 +615,8 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
                     const float2* rope, hipStream_t s) {
   EpiQKV<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
   // the grid covers rows up to roundup(M, 128) == n_pad, so the transposed V
-  // padding is written too (A rows >= M read as zero)
+  // padding is written too (A rows >= M read as zero); the Q/K/V split needs
+  // head-aligned 128-column tiles
   return launch<T>(A, lda, B, K, M, 3 * d_b, K, e, s);
 }
 
@@ -593,8 +627,19 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
                        hipStream_t s) {
   if (key_rope) {
     if (ks.head_dim > 128) return hipErrorInvalidValue;
-    EpiExpandRope<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out, key_rope};
-    return launch<T>(A, lda, B, K, M, N, K, e, s);
+    if (128 % ks.head_dim == 0) {
+      // a tile holds whole heads: the rotation is fused into the output add
+      EpiExpandRope<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out, key_rope};
+      return launch<T>(A, lda, B, K, M, N, K, e, s);
+    }
+    // heads straddle tile boundaries (head_dim 96): output add, then the
+    // rotation of every key head of the written cache
+    EpiExpand<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out};
+    hipError_t err = launch<T>(A, lda, B, K, M, N, K, e, s);
+    if (err != hipSuccess) return err;
+    const KvStrides& kd = kv_out ? ks_out : ks;
+    const int n_layers = N / (2 * ks.n_kv_heads * ks.head_dim);
+    return rotate_keys<T>(kv_out ? kv_out : kv, kd, n_layers, M, key_rope, false, 1.0f, s);
   }
   EpiExpand<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out};
   return launch<T>(A, lda, B, K, M, N, K, e, s);

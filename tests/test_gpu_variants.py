@@ -29,6 +29,16 @@ CFGS = [
          d_b=128, n_heads=2, d_seg=16),
 ]
 IDS = [f"cfg{i}" for i in range(len(CFGS))]
+# head_dim 96: heads straddle the expansion's column tiles, so global
+# placement takes the unfused path (output add, then the key rotation)
+CFGS_96 = [
+    dict(lengths=((70, 0, 133), (5, 61)), dtype="bf16", L=2, H=2, dh=96, E=128, d_c=64,
+         d_b=128, n_heads=2, d_seg=8),
+    dict(lengths=((1, 40), (33,)), dtype="f32", L=1, H=3, dh=96, E=64, d_c=64, d_b=128,
+         n_heads=4, d_seg=16),
+]
+GP_CFGS = CFGS + CFGS_96
+GP_IDS = IDS + ["dh96-bf16", "dh96-f32"]
 
 VARIANTS = {
     "token_causal": dict(mask="token_causal"),
@@ -77,7 +87,7 @@ def test_variant_parity(cfg, name):
             assert np.array_equal(Y[rows], Xs[rows])
 
 
-@pytest.mark.parametrize("cfg", CFGS, ids=IDS)
+@pytest.mark.parametrize("cfg", GP_CFGS, ids=GP_IDS)
 def test_global_placement_parity(cfg):
     from paper_2609_35139_amd.binding import Options
     w, inp, X = _case(cfg)
@@ -91,7 +101,7 @@ def test_global_placement_parity(cfg):
     assert_parity(Y, Yr, X, w)
 
 
-@pytest.mark.parametrize("cfg", CFGS, ids=IDS)
+@pytest.mark.parametrize("cfg", GP_CFGS, ids=GP_IDS)
 def test_global_placement_with_frequency_table_scale_and_output_choice(cfg):
     """Caller-supplied frequencies (a non-geometric table), a cos/sin scale,
     and V-only output: keys are rotated stale values, V is repaired."""
