@@ -124,7 +124,7 @@ struct EpiBias {
 
 template <typename T>
 struct EpiQKV {
-  static constexpr bool kWide = false;   // head-aligned Q/K/V split of 128-column tiles
+  static constexpr bool kWide = true;    // tiles stay head-aligned and inside Q, K or V
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
   template <int ROWS, int COLS, int NT>
@@ -166,7 +166,9 @@ struct EpiQKV {
       const int pc = first ? c + half : c - half;
       const int fi = first ? hc : hc - half;
       // the (cos, sin) rows of a group of passes are loaded together
-      constexpr int GRP = S::PASSES >= 4 ? 4 : S::PASSES;
+      // (fewer beside the 256x256 tile, whose other half still holds its
+      // accumulators)
+      constexpr int GRP = S::PASSES >= 4 && NT == 256 ? 4 : (S::PASSES >= 2 ? 2 : 1);
 #pragma unroll
       for (int q0 = 0; q0 < S::PASSES; q0 += GRP) {
       float4 cs[GRP][4];
@@ -578,8 +580,8 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
   return hipGetLastError();
 }
 
-// Tile choice.  bf16 products whose 256x256 tiling still fills the 256 CUs
-// take 256x256 tiles of eight waves (128x64 each, two per SIMD): half the
+// Tile choice.  bf16 products whose 256x256 tiling still keeps at least
+// three quarters of the 256 CUs busy take 256x256 tiles of eight waves (128x64 each, two per SIMD): half the
 // operand bytes per FLOP of a 128x128 tile, and one workgroup per CU with a
 // two-slab ring of 64 KB slabs.  Otherwise 128x128 tiles of four waves:
 // grids of more than one workgroup per CU use a two-slab ring (64 KB, two
@@ -593,7 +595,7 @@ static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M
                          const Epi& epi, hipStream_t s) {
   if constexpr (sizeof(T) == 2 && Epi::kWide) {
     const int64_t wide_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
-    if (wide_tiles >= 256)
+    if (4 * wide_tiles >= 3 * 256)
       return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
