@@ -599,7 +599,7 @@ static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M
       return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
-  if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
+  if (tiles <= 256) return launch_tiled<T, GemmTile<T, 2, 1, 4, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   return launch_tiled<T, GemmTile<T, 2, 2, 2>>(A, lda, B, ldb, M, N, K, epi, s);
 }
 
