@@ -581,15 +581,16 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
 }
 
 // Tile choice.  bf16 products whose 256x256 tiling still keeps at least
-// three quarters of the 256 CUs busy take 256x256 tiles of eight waves (128x64 each, two per SIMD): half the
-// operand bytes per FLOP of a 128x128 tile, and one workgroup per CU with a
-// two-slab ring of 64 KB slabs.  Otherwise 128x128 tiles of four waves:
-// grids of more than one workgroup per CU use a two-slab ring (64 KB, two
-// workgroups resident per CU hide each other's latency); grids that fit in
-// one pass over the 256 CUs use a four-slab ring instead (one workgroup per
-// CU: three slabs in flight cover the fetch latency).  Epi::kWide is false
-// for epilogues that need a 128-column tile or more registers than the
-// 256x256 tile leaves.
+// three quarters of the 256 CUs busy take 256x256 tiles of eight waves
+// (128x64 each, two per SIMD): half the operand bytes per FLOP of a 128x128
+// tile, and one workgroup per CU with a two-slab ring of 64 KB slabs.
+// Otherwise 128x128 tiles: grids of more than one workgroup per CU use four
+// waves (64x64 each) and a two-slab ring (64 KB, two workgroups resident per
+// CU hide each other's latency); grids that fit in one pass over the 256 CUs
+// use eight waves (64x32 each, so two per SIMD) and a four-slab ring (three
+// slabs in flight cover the fetch latency).  Epi::kWide is false for
+// epilogues that need a 128-column tile or more registers than the 256x256
+// tile leaves.
 template <typename T, typename Epi>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                          const Epi& epi, hipStream_t s) {
