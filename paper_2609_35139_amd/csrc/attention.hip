@@ -248,7 +248,8 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     // row sum is taken over the packed values the product uses
     frag pb[2][PS];
     auto probs = [&](auto shifted, float shift) {
-      float ts = 0.f;
+      // one partial sum per fragment, so the dot2 chains are independent
+      float tp[2][PS];
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
@@ -259,8 +260,13 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
             pv[e] = __builtin_amdgcn_exp2f(decltype(shifted)::value ? s[rt][s2 * KPL + e] - shift
                                                                     : s[rt][s2 * KPL + e]);
           pb[rt][s2] = pack_frag(pv, (frag*)nullptr);
-          ts = frag_sum(pb[rt][s2], ts);
+          tp[rt][s2] = frag_sum(pb[rt][s2], 0.f);
         }
+      float ts = 0.f;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int s2 = 0; s2 < PS; ++s2) ts += tp[rt][s2];
       return ts;
     };
     // Fast path: the reference max stays where it is.  A probability is at

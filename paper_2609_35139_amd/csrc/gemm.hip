@@ -38,6 +38,8 @@ struct GemmTile {
   static constexpr int STAGE_BYTES = (BM + BN) * 128;
   static constexpr int LDC = BN + 4;                // fp32 staging row (16-byte aligned rows)
   static constexpr int EPI_ROWS = BM > 128 ? BM / 2 : BM;
+  // a single staging pass issues its epilogue loads before the main loop
+  static constexpr bool EARLY = EPI_ROWS == BM;
   static constexpr size_t LDS_MAIN = (size_t)STAGES * STAGE_BYTES;
   static constexpr size_t LDS_C = (size_t)EPI_ROWS * LDC * sizeof(float);
   static constexpr size_t LDS = LDS_MAIN > LDS_C ? LDS_MAIN : LDS_C;
@@ -495,12 +497,11 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 
   // the epilogue's global loads (bias, residuals, the stale cache) go out
   // before the main loop and land while it runs
-  // (one staging pass: before the main loop, where they land while it runs;
-  // two passes: before each pass, so the loop keeps its registers)
+  // (a single staging pass: before the main loop, where they land while it
+  // runs; two passes: before each pass, so the loop keeps its registers)
   constexpr int ER = G::EPI_ROWS;
-  constexpr bool kEarly = ER == G::BM;
   typename Epi::template Pre<ER, G::BN, G::NT> pre;
-  if constexpr (kEarly) epi.template prefetch<ER, G::BN, G::NT>(pre, m0, n0, M, N);
+  if constexpr (G::EARLY) epi.template prefetch<ER, G::BN, G::NT>(pre, m0, n0, M, N);
 
   f32x16 acc[G::TM][G::TN];
 #pragma unroll
@@ -548,7 +549,7 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   float* Cs = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int part = 0; part < G::BM / ER; ++part) {
-    if constexpr (!kEarly) epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
+    if (part > 0 || !G::EARLY) epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
     __syncthreads();  // ring (or the previous pass's rows) no longer read
 #pragma unroll
     for (int i = 0; i < G::TM; ++i) {
