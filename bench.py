@@ -26,7 +26,7 @@ FUNCTION_OF = {
     "gemm_compress": "gemm_nt_kernel<EpiBias>", "gemm_token": "gemm_nt_kernel<EpiBias>",
     "gemm_fuse": "gemm_nt_kernel<EpiBias>", "gemm_inject": "gemm_nt_kernel<EpiBias>",
     "gemm_oproj": "gemm_nt_kernel<EpiBias>", "gemm_ffn1": "gemm_nt_kernel<EpiBias>",
-    "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKV>",
+    "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKVh>",
     "gemm_expand": "gemm_nt_kernel<EpiExpand>", "attention": "attention_kernel",
     "layernorm": "layernorm_kernel", "compress_segments": "compress_segments_kernel",
     "schedule": "schedule_kernel", "rope_table": "rope_table_kernel",

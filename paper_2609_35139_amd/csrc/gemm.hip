@@ -70,6 +70,7 @@ __device__ __forceinline__ void load8f(const float* p, float* v) {
 
 template <typename T>
 struct EpiBias {
+  __device__ int b_row(int n) const { return n; }   // output column -> weight row
   static constexpr bool kWide = true;
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
   int64_t ldr2; int gelu;
@@ -124,100 +125,83 @@ struct EpiBias {
   }
 };
 
+// QKV projection with the output columns taken head by head: tile column
+// n is weight row b_row(n), so that columns [3*d_head*h, 3*d_head*(h+1))
+// hold Q, K and V of head h.  A 192-column tile then holds whole heads
+// (d_head 32 or 64) and a 256x192 tiling of the headline shape is exactly
+// one tile per CU.  Q and K get the backbone's RoPE (Q also the scale into
+// exp2 units) and are written row-major; V is written transposed.  K rows
+// and V^T columns in [M, n_pad) get finite values from clamped A rows.
 template <typename T>
-struct EpiQKV {
-  static constexpr bool kWide = true;    // tiles stay head-aligned and inside Q, K or V
+struct EpiQKVh {
+  static constexpr bool kWide = true;
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
   const float2* rope;
-  template <int ROWS, int COLS, int NT>
-  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS, NT>::PASSES]; };
-  template <int ROWS, int COLS, int NT>
-  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
-    if (n0 >= 2 * d_b) return;      // V tiles load their bias per column in run()
-    using S = SegMap<ROWS, COLS, NT>;
-    const int half = d_head / 2;
-    const int c = S::col(), hc = c % d_head;
-    const int pc = hc < half ? c + half : c - half;
-    load8f(bias + n0 + c, p.bx);
-    load8f(bias + n0 + pc, p.by);
-#pragma unroll
-    for (int q = 0; q < S::PASSES; ++q) {
-      const int gm = m0 + S::row(q);
-      p.pp[q] = gm < M ? pos[gm] : 0;
-    }
+  __device__ int b_row(int n) const {
+    const int g3 = 3 * d_head, rem = n % g3;
+    return (rem / d_head) * d_b + (n / g3) * d_head + rem % d_head;
   }
+  template <int ROWS, int COLS, int NT>
+  struct Pre {};
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>&, int, int, int, int) const {}
   template <int ROWS, int COLS, int LDC, int NT>
-  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& p, int m0, int n0, int M,
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>&, int m0, int n0, int M,
                       int N) const {
-    if (n0 < 2 * d_b) {
-      // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
-      // The tile is head-aligned and never straddles Q/K (d_b % COLS == 0).
-      // Q leaves scaled by log2(e)/sqrt(d_head) (the attention works in exp2
-      // units); K rows in [M, n_pad) get finite values from clamped rows
-      // (padding read by the attention's last key tile).
-      using S = SegMap<ROWS, COLS, NT>;
-      const bool is_q = n0 < d_b;
-      T* dst = is_q ? q : k;
-      const int rows_out = is_q ? M : (int)n_pad;
-      const float osc = is_q ? 1.4426950408889634f / __builtin_sqrtf((float)d_head) : 1.0f;
-      const int cbase = n0 < d_b ? n0 : n0 - d_b;
-      const int half = d_head / 2;
-      const int c = S::col();
-      const int hc = c % d_head;
-      const bool first = hc < half;
-      const int pc = first ? c + half : c - half;
-      const int fi = first ? hc : hc - half;
-      // the (cos, sin) rows of a group of passes are loaded together
-      // (fewer beside the 256x256 tile, whose other half still holds its
-      // accumulators)
-      constexpr int GRP = S::PASSES >= 4 && NT == 256 ? 4 : (S::PASSES >= 2 ? 2 : 1);
+    const int g3 = 3 * d_head, half = d_head / 2;
+    const int groups = COLS / g3;                       // heads in the tile
+    // Q and K: 8-column segments, both members of every rotate-half pair
+    const int qk_segs = groups * (2 * d_head / 8);
+    const float qsc = 1.4426950408889634f / __builtin_sqrtf((float)d_head);
+    for (int idx = threadIdx.x; idx < ROWS * qk_segs; idx += NT) {
+      const int r = idx / qk_segs, sg = idx % qk_segs;
+      const int grp = sg / (2 * d_head / 8), w = (sg % (2 * d_head / 8)) * 8;  // w in [0, 2 d_head)
+      const int part = w / d_head, i = w % d_head;
+      const int c = grp * g3 + w;                       // tile column
+      const int hh = (n0 + c) / g3;
+      const bool is_q = part == 0;
+      const int gm = m0 + r;
+      if (gm >= (is_q ? M : (int)n_pad) || n0 + c >= N) continue;
+      const bool first = i < half;
+      const int pi = first ? i + half : i - half;       // partner index in the head
+      const int fi = first ? i : i - half;
+      float x[8], y[8], bx[8], by[8];
+      load8f(Cs + r * LDC + c, x);
+      load8f(Cs + r * LDC + c - i + pi, y);
+      const int bcol = part * d_b + hh * d_head;
+      load8f(bias + bcol + i, bx);
+      load8f(bias + bcol + pi, by);
+      const int p = gm < M ? pos[gm] : 0;
+      const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)p * half + fi);
+      const float osc = is_q ? qsc : 1.0f;
+      float v[8];
 #pragma unroll
-      for (int q0 = 0; q0 < S::PASSES; q0 += GRP) {
-      float4 cs[GRP][4];
-#pragma unroll
-      for (int q = 0; q < GRP; ++q) {
-        const float4* t4 =
-            reinterpret_cast<const float4*>(rope + (int64_t)p.pp[q0 + q] * half + fi);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
+      for (int e = 0; e < 4; ++e) {
+        const float4 t = t4[e];   // (cos, sin) of pairs 2e and 2e+1
+        const float x0 = x[2 * e] + bx[2 * e], y0 = y[2 * e] + by[2 * e];
+        const float x1 = x[2 * e + 1] + bx[2 * e + 1], y1 = y[2 * e + 1] + by[2 * e + 1];
+        v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
+        v[2 * e + 1] = (first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w) * osc;
       }
+      Vec8<T> o; o.from_float(v);
+      o.store((is_q ? q : k) + (int64_t)gm * d_b + hh * d_head + i);
+    }
+    // V: transposed, vt[head][d][token], 8 tokens per 16-byte store;
+    // consecutive threads take consecutive columns (conflict-free LDS reads)
+    const int v_cols = groups * d_head;
+    for (int idx = threadIdx.x; idx < v_cols * (ROWS / 8); idx += NT) {
+      const int vc = idx % v_cols, r = (idx / v_cols) * 8;
+      const int grp = vc / d_head, i = vc % d_head;
+      const int c = grp * g3 + 2 * d_head + i;
+      const int gn = n0 + c, gm = m0 + r;
+      if (gn >= N || gm + 8 > n_pad) continue;
+      const int hh = gn / g3;
+      const float bb = bias[2 * d_b + hh * d_head + i];
+      float v[8];
 #pragma unroll
-      for (int q = 0; q < GRP; ++q) {
-        const int qq = q0 + q;
-        const int r = S::row(qq), gm = m0 + r;
-        if (gm >= rows_out) continue;
-        float x[8], y[8], v[8];
-        load8f(Cs + r * LDC + c, x);
-        load8f(Cs + r * LDC + pc, y);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
-          const float x0 = x[2 * e] + p.bx[2 * e], y0 = y[2 * e] + p.by[2 * e];
-          const float x1 = x[2 * e + 1] + p.bx[2 * e + 1], y1 = y[2 * e + 1] + p.by[2 * e + 1];
-          v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
-          v[2 * e + 1] = (first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w) * osc;
-        }
-        Vec8<T> o; o.from_float(v); o.store(dst + (int64_t)gm * d_b + cbase + c);
-      }
-      }
-    } else {
-      // V: written transposed, vt[head][d][token], 8 tokens per 16-byte
-      // store.  Consecutive threads take consecutive columns, so the column
-      // reads of the staged tile are conflict-free.  Rows in [M, n_pad) hold
-      // values computed from clamped rows: finite padding.
-      constexpr int RSEG = ROWS / 8;
-      for (int idx = threadIdx.x; idx < COLS * RSEG; idx += NT) {
-        const int c = idx % COLS, r = (idx / COLS) * 8;
-        const int gn = n0 + c, gm = m0 + r;
-        if (gn >= N || gm + 8 > n_pad) continue;
-        const int vc = gn - 2 * d_b;
-        const float bb = bias[gn];
-        float v[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + c] + bb;
-        Vec8<T> o; o.from_float(v);
-        o.store(vt + (int64_t)vc * n_pad + gm);
-      }
+      for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + c] + bb;
+      Vec8<T> o; o.from_float(v);
+      o.store(vt + (int64_t)(hh * d_head + i) * n_pad + gm);
     }
   }
 };
@@ -236,6 +220,7 @@ __device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* 
 
 template <typename T>
 struct EpiExpand {
+  __device__ int b_row(int n) const { return n; }   // output column -> weight row
   // 128x128 tiles: the stale-cache loads are issued before the main loop
   // (measured faster than 256x256 tiles, whose loads wait for the loop's end)
   static constexpr bool kWide = false;
@@ -313,6 +298,7 @@ struct EpiExpand {
 // straddles two 128-column tiles).
 template <typename T>
 struct EpiExpandRope {
+  __device__ int b_row(int n) const { return n; }   // output column -> weight row
   static constexpr bool kWide = false;   // pair registers do not fit beside a 256x256 tile
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
@@ -484,7 +470,8 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   for (int r = 0; r < G::B_ROUNDS; ++r) {
     const int row = (r * G::NW + wave) * 8 + (lane >> 3);
     const int chunk = (lane & 7) ^ swz128(row);
-    bsrc[r] = reinterpret_cast<const char*>(B + (int64_t)min(n0 + row, N - 1) * ldb) + chunk * 16;
+    bsrc[r] = reinterpret_cast<const char*>(B + (int64_t)epi.b_row(min(n0 + row, N - 1)) * ldb) +
+              chunk * 16;
   }
   auto issue = [&](int kt, int stage) {
     char* base = smem + stage * G::STAGE_BYTES;
@@ -617,11 +604,19 @@ template <typename T>
 hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
                     T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
                     const float2* rope, hipStream_t s) {
-  EpiQKV<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
-  // the grid covers rows up to roundup(M, 128) == n_pad, so the transposed V
-  // padding is written too (A rows >= M read as zero); the Q/K/V split needs
-  // head-aligned 128-column tiles
-  return launch<T>(A, lda, B, K, M, 3 * d_b, K, e, s);
+  if (192 % (3 * d_head) != 0 || (3 * d_b) % 192 != 0) return hipErrorInvalidValue;
+  EpiQKVh<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
+  // 192-column tiles of whole heads: 256x192 on eight waves (64x96 each) when
+  // that grid keeps three quarters of the CUs busy, else 128x192 on four.
+  // The grid covers rows up to roundup(M, 128) >= n_pad, so the transposed V
+  // padding is written too (A rows >= M are clamped copies: finite).
+  const int N = 3 * d_b;
+  if constexpr (sizeof(T) == 2) {
+    const int64_t wide = (int64_t)((M + 255) / 256) * (N / 192);
+    if (4 * wide >= 3 * 256)
+      return launch_tiled<T, GemmTile<T, 2, 3, 2, 4, 2>>(A, lda, B, K, M, N, K, e, s);
+  }
+  return launch_tiled<T, GemmTile<T, 2, 3, 3, 2, 2>>(A, lda, B, K, M, N, K, e, s);
 }
 
 template <typename T>

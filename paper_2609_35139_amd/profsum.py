@@ -33,7 +33,7 @@ CLASS_KERNEL = {
     "layernorm": ("layernorm_kernel", ["rowops.hip", "common.h", "launch.h"]),
     "compress_segments": ("compress_segments_kernel", ["rowops.hip", "common.h", "launch.h"]),
     "gemm_expand": ("EpiExpand", ["gemm.hip", "common.h", "launch.h"]),
-    "gemm_qkv": ("EpiQKV", ["gemm.hip", "common.h", "launch.h"]),
+    "gemm_qkv": ("EpiQKVh", ["gemm.hip", "common.h", "launch.h"]),
 }
 for _c in ("gemm_compress", "gemm_token", "gemm_fuse", "gemm_inject", "gemm_oproj", "gemm_ffn1",
            "gemm_ffn2"):
@@ -58,7 +58,7 @@ def bench_line(path):
 
 def short_name(n):
     n = re.sub(r"\(.*", "", n)
-    for k in ("EpiBias", "EpiQKV", "EpiExpand"):
+    for k in ("EpiBias", "EpiQKVh", "EpiExpandRope", "EpiExpand"):
         if k in n:
             return "gemm_nt_kernel<" + k + ">"
     m = re.search(r"cr::(\w+)|_ZN2cr\d+(\w+?)I|_ZN2cr\d+(\w+)E", n)
