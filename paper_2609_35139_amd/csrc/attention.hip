@@ -48,8 +48,10 @@ struct AttnCfg {
   static constexpr int OPS = K_ROUNDS + V_ROUNDS;     // DMA ops per thread per tile
   static constexpr int STAGE_BYTES = K_BYTES + V_BYTES;
   static constexpr int RING_BYTES = STAGES * STAGE_BYTES;
-  // merge area: group 1 hands (m, l, O^T) of its 128 queries to group 0
-  static constexpr int MERGE_BYTES = BQ * D * 4 + 2 * BQ * 2 * 4;
+  // merge area: group 1 hands (m, l, O^T) of its 128 queries to group 0;
+  // rows of D + 1 floats, so the 32 queries of a wave fall in distinct banks
+  static constexpr int MLD = D + 1;
+  static constexpr int MERGE_BYTES = BQ * MLD * 4 + 2 * BQ * 2 * 4;
   static constexpr int LDS = GROUPS * RING_BYTES > MERGE_BYTES ? GROUPS * RING_BYTES : MERGE_BYTES;
 };
 
@@ -324,15 +326,15 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   // merge group 1 into group 0: per query q' = gw*32 + ql, lane half g holds
   // l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4 of O^T
   __syncthreads();   // both rings idle
-  float* mo = reinterpret_cast<float*>(lds);                  // [BQ][D] O^T values
-  float* ml = mo + C::BQ * D;                                 // [BQ][2] (m, l) per lane half
+  float* mo = reinterpret_cast<float*>(lds);                  // [BQ][MLD] O^T values
+  float* ml = mo + C::BQ * C::MLD;                            // [BQ][2] (m, l) per lane half
   const int qrow = gw * 32 + ql;
   if (grp == 1) {
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
       for (int v = 0; v < 16; ++v)
-        mo[qrow * D + d * 32 + (v >> 2) * 8 + g * 4 + (v & 3)] = oacc[d][v];
+        mo[qrow * C::MLD + d * 32 + (v >> 2) * 8 + g * 4 + (v & 3)] = oacc[d][v];
     ml[(qrow * 2 + g) * 2 + 0] = m_ref;
     ml[(qrow * 2 + g) * 2 + 1] = lsum;
   }
@@ -354,7 +356,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
       T outv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        outv[e] = from_f32<T>((oacc[d][i4 * 4 + e] * a0 + mo[qrow * D + dd + e] * a1) * inv);
+        outv[e] = from_f32<T>((oacc[d][i4 * 4 + e] * a0 + mo[qrow * C::MLD + dd + e] * a1) * inv);
       if constexpr (sizeof(T) == 2) {
         *reinterpret_cast<uint2*>(orow + dd) = *reinterpret_cast<const uint2*>(outv);
       } else {
