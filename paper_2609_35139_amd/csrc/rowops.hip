@@ -119,7 +119,10 @@ __global__ __launch_bounds__(256) void compress_segments_kernel(
   constexpr int NK = DH / MM::KSTEP;
   constexpr int TOK = 16 * TB;
   constexpr int VE = 16 / (int)sizeof(T);
-  __shared__ __align__(16) T stage[TOK * 128];   // [token][4 segments x <= 32 columns]
+  // [token][4 segments x <= 32 columns]; rows padded by 16 bytes so that the
+  // 16 tokens written together fall in distinct LDS banks
+  constexpr int LDST = 128 + 16 / (int)sizeof(T);
+  __shared__ __align__(16) T stage[TOK * LDST];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g0 = blockIdx.y * 4, g = g0 + wave;
   const int span = min(4, S - g0) * d_seg;
@@ -165,7 +168,7 @@ __global__ __launch_bounds__(256) void compress_segments_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int c = j * 16 + (lane >> 4) * 4 + e;
-          if (c < d_seg) stage[r * 128 + wave * d_seg + c] = from_f32<T>(acc[j][e] + bb[j][e]);
+          if (c < d_seg) stage[r * LDST + wave * d_seg + c] = from_f32<T>(acc[j][e] + bb[j][e]);
         }
     }
   }
@@ -178,12 +181,12 @@ __global__ __launch_bounds__(256) void compress_segments_kernel(
       const int r = i / cpr, c = (i % cpr) * VE, t = t0 + r;
       if (t < N)
         *reinterpret_cast<uint4*>(U + (int64_t)t * ldu + col0 + c) =
-            *reinterpret_cast<const uint4*>(stage + r * 128 + c);
+            *reinterpret_cast<const uint4*>(stage + r * LDST + c);
     }
   } else {
     for (int i = threadIdx.x; i < TOK * span; i += 256) {
       const int r = i / span, c = i % span, t = t0 + r;
-      if (t < N) U[(int64_t)t * ldu + col0 + c] = stage[r * 128 + c];
+      if (t < N) U[(int64_t)t * ldu + col0 + c] = stage[r * LDST + c];
     }
   }
   if (blockIdx.y == 0) {  // zero the K padding of U for these tokens
