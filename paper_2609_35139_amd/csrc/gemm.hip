@@ -125,6 +125,107 @@ struct EpiBias {
   }
 };
 
+// QKV projection in the weights' own column order [Q | K | V] on 128-column
+// tiles (each inside Q, K or V and head-aligned, d_b % 128 == 0).
+template <typename T>
+struct EpiQKV {
+  static constexpr bool kWide = false;   // head-aligned 128-column tiles
+  __device__ int b_row(int n) const { return n; }   // output column -> weight row
+  T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
+  const float2* rope;
+  template <int ROWS, int COLS, int NT>
+  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS, NT>::PASSES]; };
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
+    if (n0 >= 2 * d_b) return;      // V tiles load their bias per column in run()
+    using S = SegMap<ROWS, COLS, NT>;
+    const int half = d_head / 2;
+    const int c = S::col(), hc = c % d_head;
+    const int pc = hc < half ? c + half : c - half;
+    load8f(bias + n0 + c, p.bx);
+    load8f(bias + n0 + pc, p.by);
+#pragma unroll
+    for (int q = 0; q < S::PASSES; ++q) {
+      const int gm = m0 + S::row(q);
+      p.pp[q] = gm < M ? pos[gm] : 0;
+    }
+  }
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& p, int m0, int n0, int M,
+                      int N) const {
+    if (n0 < 2 * d_b) {
+      // Q or K: rotate pairs (i, i + d_head/2) of every head by pos * freq_i.
+      // The tile is head-aligned and never straddles Q/K (d_b % COLS == 0).
+      // Q leaves scaled by log2(e)/sqrt(d_head) (the attention works in exp2
+      // units); K rows in [M, n_pad) get finite values from clamped rows
+      // (padding read by the attention's last key tile).
+      using S = SegMap<ROWS, COLS, NT>;
+      const bool is_q = n0 < d_b;
+      T* dst = is_q ? q : k;
+      const int rows_out = is_q ? M : (int)n_pad;
+      const float osc = is_q ? 1.4426950408889634f / __builtin_sqrtf((float)d_head) : 1.0f;
+      const int cbase = n0 < d_b ? n0 : n0 - d_b;
+      const int half = d_head / 2;
+      const int c = S::col();
+      const int hc = c % d_head;
+      const bool first = hc < half;
+      const int pc = first ? c + half : c - half;
+      const int fi = first ? hc : hc - half;
+      // the (cos, sin) rows of a group of passes are loaded together
+      // (fewer beside the 256x256 tile, whose other half still holds its
+      // accumulators)
+      constexpr int GRP = S::PASSES >= 4 && NT == 256 ? 4 : (S::PASSES >= 2 ? 2 : 1);
+#pragma unroll
+      for (int q0 = 0; q0 < S::PASSES; q0 += GRP) {
+      float4 cs[GRP][4];
+#pragma unroll
+      for (int q = 0; q < GRP; ++q) {
+        const float4* t4 =
+            reinterpret_cast<const float4*>(rope + (int64_t)p.pp[q0 + q] * half + fi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
+      }
+#pragma unroll
+      for (int q = 0; q < GRP; ++q) {
+        const int qq = q0 + q;
+        const int r = S::row(qq), gm = m0 + r;
+        if (gm >= rows_out) continue;
+        float x[8], y[8], v[8];
+        load8f(Cs + r * LDC + c, x);
+        load8f(Cs + r * LDC + pc, y);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float4 t = cs[q][e];   // (cos, sin) of pairs 2e and 2e+1
+          const float x0 = x[2 * e] + p.bx[2 * e], y0 = y[2 * e] + p.by[2 * e];
+          const float x1 = x[2 * e + 1] + p.bx[2 * e + 1], y1 = y[2 * e + 1] + p.by[2 * e + 1];
+          v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
+          v[2 * e + 1] = (first ? x1 * t.z - y1 * t.w : x1 * t.z + y1 * t.w) * osc;
+        }
+        Vec8<T> o; o.from_float(v); o.store(dst + (int64_t)gm * d_b + cbase + c);
+      }
+      }
+    } else {
+      // V: written transposed, vt[head][d][token], 8 tokens per 16-byte
+      // store.  Consecutive threads take consecutive columns, so the column
+      // reads of the staged tile are conflict-free.  Rows in [M, n_pad) hold
+      // values computed from clamped rows: finite padding.
+      constexpr int RSEG = ROWS / 8;
+      for (int idx = threadIdx.x; idx < COLS * RSEG; idx += NT) {
+        const int c = idx % COLS, r = (idx / COLS) * 8;
+        const int gn = n0 + c, gm = m0 + r;
+        if (gn >= N || gm + 8 > n_pad) continue;
+        const int vc = gn - 2 * d_b;
+        const float bb = bias[gn];
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + c] + bb;
+        Vec8<T> o; o.from_float(v);
+        o.store(vt + (int64_t)vc * n_pad + gm);
+      }
+    }
+  }
+};
+
 // QKV projection with the output columns taken head by head: tile column
 // n is weight row b_row(n), so that columns [3*d_head*h, 3*d_head*(h+1))
 // hold Q, K and V of head h.  A 192-column tile then holds whole heads
@@ -568,8 +669,8 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
   return hipGetLastError();
 }
 
-// Tile choice.  bf16 products whose 256x256 tiling still keeps at least
-// three quarters of the 256 CUs busy take 256x256 tiles of eight waves
+// Tile choice.  bf16 products whose 256x256 tiling fills its rounds well
+// enough (round_fill, kWideGain) take 256x256 tiles of eight waves
 // (128x64 each, two per SIMD): half the operand bytes per FLOP of a 128x128
 // tile, and one workgroup per CU with a two-slab ring of 64 KB slabs.
 // Otherwise 128x128 tiles: grids of more than one workgroup per CU use four
@@ -579,12 +680,25 @@ static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb,
 // slabs in flight cover the fetch latency).  Epi::kWide is false for
 // epilogues that need a 128-column tile or more registers than the 256x256
 // tile leaves.
+// Fraction of the workgroup slots busy over the rounds a grid of `tiles`
+// takes on `slots` resident workgroups.
+static inline double round_fill(int64_t tiles, int64_t slots) {
+  const int64_t rounds = (tiles + slots - 1) / slots;
+  return rounds > 0 ? (double)tiles / (double)(rounds * slots) : 0.0;
+}
+// A 256-row tile's main loop moves about 1.25x the FLOPs of a 128x128 tile
+// per unit time (half the operand bytes per FLOP), so it is taken when that
+// outweighs a worse fill of the last round.
+constexpr double kWideGain = 1.25;
+
 template <typename T, typename Epi>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
                          const Epi& epi, hipStream_t s) {
   if constexpr (sizeof(T) == 2 && Epi::kWide) {
     const int64_t wide_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
-    if (4 * wide_tiles >= 3 * 256)
+    const int64_t tiles128 = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+    const double fill128 = tiles128 <= 256 ? round_fill(tiles128, 256) : round_fill(tiles128, 512);
+    if (kWideGain * round_fill(wide_tiles, 256) >= fill128)
       return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
   }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
@@ -604,19 +718,23 @@ template <typename T>
 hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
                     T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
                     const float2* rope, hipStream_t s) {
-  if (192 % (3 * d_head) != 0 || (3 * d_b) % 192 != 0) return hipErrorInvalidValue;
-  EpiQKVh<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
-  // 192-column tiles of whole heads: 256x192 on eight waves (64x96 each) when
-  // that grid keeps three quarters of the CUs busy, else 128x192 on four.
-  // The grid covers rows up to roundup(M, 128) >= n_pad, so the transposed V
-  // padding is written too (A rows >= M are clamped copies: finite).
   const int N = 3 * d_b;
+  // 192-column tiles of whole heads on a 256x192 grid (eight waves of 64x96)
+  // when it fills its rounds well enough; otherwise 128x128 tiles in the
+  // weights' own column order.  Either grid covers rows up to roundup(M, 128)
+  // >= n_pad, so the transposed V padding is written too (A rows >= M are
+  // clamped copies: finite).
   if constexpr (sizeof(T) == 2) {
     const int64_t wide = (int64_t)((M + 255) / 256) * (N / 192);
-    if (4 * wide >= 3 * 256)
+    const int64_t tiles128 = (int64_t)((M + 127) / 128) * (N / 128);
+    const double fill128 = tiles128 <= 256 ? round_fill(tiles128, 256) : round_fill(tiles128, 512);
+    if (192 % (3 * d_head) == 0 && N % 192 == 0 && kWideGain * round_fill(wide, 256) >= fill128) {
+      EpiQKVh<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
       return launch_tiled<T, GemmTile<T, 2, 3, 2, 4, 2>>(A, lda, B, K, M, N, K, e, s);
+    }
   }
-  return launch_tiled<T, GemmTile<T, 2, 3, 3, 2, 2>>(A, lda, B, K, M, N, K, e, s);
+  EpiQKV<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
+  return launch<T>(A, lda, B, K, M, N, K, e, s);
 }
 
 template <typename T>
