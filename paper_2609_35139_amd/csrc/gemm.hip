@@ -611,22 +611,46 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 
     const char* as = smem + (kt % G::STAGES) * G::STAGE_BYTES;
     const char* bs = as + G::BM * 128;
-#pragma unroll
-    for (int ks = 0; ks < G::BK; ks += MM::KSTEP) {
-      const int k = ks + (lane >> 5) * MM::KPL;
+    // fragments double-buffered across the slab's k-steps: the reads of step
+    // ks + 1 are issued between the products of step ks
+    constexpr int NKS = G::BK / MM::KSTEP;
+    frag af[2][G::TM], bfr[2][G::TN];
+    auto ld = [&](int ks, int buf) {
+      const int k = ks * MM::KSTEP + (lane >> 5) * MM::KPL;
       const int cofs = (((k / G::VEC) ^ fsw) << 4) + (k % G::VEC) * (int)sizeof(T);
-      frag af[G::TM], bfr[G::TN];
 #pragma unroll
       for (int i = 0; i < G::TM; ++i)
-        af[i] = *reinterpret_cast<const frag*>(as + (wm + i * 32 + fr) * 128 + cofs);
+        af[buf][i] = *reinterpret_cast<const frag*>(as + (wm + i * 32 + fr) * 128 + cofs);
 #pragma unroll
       for (int j = 0; j < G::TN; ++j)
-        bfr[j] = *reinterpret_cast<const frag*>(bs + (wn + j * 32 + fr) * 128 + cofs);
+        bfr[buf][j] = *reinterpret_cast<const frag*>(bs + (wn + j * 32 + fr) * 128 + cofs);
+    };
+    ld(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      if (ks + 1 < NKS) ld(ks + 1, (ks + 1) & 1);
 #pragma unroll
       for (int i = 0; i < G::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < G::TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
+        for (int j = 0; j < G::TN; ++j)
+          acc[i][j] = MM::mma(bfr[ks & 1][j], af[ks & 1][i], acc[i][j]);
     }
+    // instruction order for the scheduler: the first step's LDS reads, then
+    // every step's MFMAs alternating with the next step's reads
+    constexpr int NR = G::TM + G::TN, NM = G::TM * G::TN;
+    constexpr int NP = NR < NM ? NR : NM;
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);        // DS reads
+#pragma unroll
+    for (int ks = 0; ks + 1 < NKS; ++ks) {
+#pragma unroll
+      for (int r = 0; r < NP; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
+      if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
   }
 
   // Epilogue.  With the weight tile as the MFMA's first operand, lane l of
