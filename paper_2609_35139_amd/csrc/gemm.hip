@@ -24,9 +24,13 @@ namespace cr {
 // of one 128-byte row per tile row; STAGES slabs live in the LDS ring.  The
 // fp32 output tile is staged through LDS over the ring, EPI_ROWS rows at a
 // time (the whole tile, or half of it for 256-row tiles).
-template <typename T, int TM_, int TN_, int STAGES_, int WGM_ = 2, int WGN_ = 2>
+template <typename T, int TM_, int TN_, int STAGES_, int WGM_ = 2, int WGN_ = 2,
+          bool EARLY2_ = false>
 struct GemmTile {
   static constexpr int TM = TM_, TN = TN_, STAGES = STAGES_, WGM = WGM_, WGN = WGN_;
+  // two staging passes: the first pass's epilogue loads go out before the
+  // main loop too
+  static constexpr bool EARLY2 = EARLY2_;
   static constexpr int NW = WGM * WGN, NT = 64 * NW;
   static constexpr int WM = 32 * TM, WN = 32 * TN;
   static constexpr int BM = WGM * WM, BN = WGN * WN;
@@ -322,16 +326,19 @@ __device__ __forceinline__ T* kv_coord(T* kv, const KvStrides& ks, int j, bool* 
 template <typename T>
 struct EpiExpand {
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
-  // 128x128 tiles: the stale-cache loads are issued before the main loop
-  // (measured faster than 256x256 tiles, whose loads wait for the loop's end)
   static constexpr bool kWide = false;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
+  // What the prefetch holds: the stale values of the thread's rows and a
+  // bitmask of its kept rows; bias and sigma (two 8-float column vectors)
+  // are loaded in run() beside a 256x256 tile, whose main loop leaves no
+  // registers for them, and prefetched otherwise.
   template <int ROWS, int COLS, int NT>
   struct Pre {
-    float b[8], sg[8];
+    static constexpr bool kVec = NT == 256;
+    float b[kVec ? 8 : 1], sg[kVec ? 8 : 1];
     Vec8<T> x[SegMap<ROWS, COLS, NT>::PASSES];
-    int kp[SegMap<ROWS, COLS, NT>::PASSES];
+    unsigned kbits;
   };
   // 8 | d_h keeps a segment in one head
   __device__ bool selected(int gn, T** base) const {
@@ -342,20 +349,24 @@ struct EpiExpand {
   template <int ROWS, int COLS, int NT>
   __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
     using S = SegMap<ROWS, COLS, NT>;
+    static_assert(S::PASSES <= 32, "keep bitmask");
     const int gn = n0 + S::col();
+    p.kbits = 0;
     if (gn >= N) return;
     T* base;
     const bool sel = selected(gn, &base);
     if (!sel && !kvo) return;                      // unselected component: left stale in place
-    if (sel) {
-      load8f(bias + gn, p.b);
-      load8f(sigma + gn, p.sg);
+    if constexpr (Pre<ROWS, COLS, NT>::kVec) {
+      if (sel) {
+        load8f(bias + gn, p.b);
+        load8f(sigma + gn, p.sg);
+      }
     }
     const bool need_x = kvo || (mode & EXPAND_RESIDUAL);
 #pragma unroll
     for (int q = 0; q < S::PASSES; ++q) {
       const int gm = m0 + S::row(q);
-      p.kp[q] = (gm < M && keep) ? keep[gm] : 0;
+      if (gm < M && keep && keep[gm]) p.kbits |= 1u << q;
       if (gm < M && need_x) p.x[q].load(base + ks.tok(gm));
     }
   }
@@ -370,6 +381,14 @@ struct EpiExpand {
     bool dummy;
     T* obase = kvo ? kv_coord(kvo, kso, gn, &dummy) : base;
     const bool res = mode & EXPAND_RESIDUAL;
+    float bv[8], sv[8];
+    if constexpr (Pre<ROWS, COLS, NT>::kVec) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { bv[e] = p.b[e]; sv[e] = p.sg[e]; }
+    } else if (sel) {
+      load8f(bias + gn, bv);
+      load8f(sigma + gn, sv);
+    }
 #pragma unroll
     for (int q = 0; q < S::PASSES; ++q) {
       const int r = S::row(q), gm = m0 + r;
@@ -377,7 +396,7 @@ struct EpiExpand {
       // (no reference that selects between the two stride sets: it would pin
       // the epilogue's arguments to scratch memory)
       const int64_t to = kvo ? kso.tok(gm) : ks.tok(gm);
-      if (!sel || p.kp[q]) {                       // stale values: copied when out of place
+      if (!sel || (p.kbits >> q & 1u)) {           // stale values: copied when out of place
         if (kvo) p.x[q].store(obase + to);
         continue;
       }
@@ -385,7 +404,7 @@ struct EpiExpand {
       load8f(Cs + r * LDC + c, a);
       if (res) p.x[q].to_float(f);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + p.sg[e] * (a[e] + p.b[e]);
+      for (int e = 0; e < 8; ++e) f[e] = (res ? f[e] : 0.f) + sv[e] * (a[e] + bv[e]);
       p.x[q].from_float(f);
       p.x[q].store(obase + to);
     }
@@ -589,7 +608,7 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   // runs; two passes: before each pass, so the loop keeps its registers)
   constexpr int ER = G::EPI_ROWS;
   typename Epi::template Pre<ER, G::BN, G::NT> pre;
-  if constexpr (G::EARLY) epi.template prefetch<ER, G::BN, G::NT>(pre, m0, n0, M, N);
+  if constexpr (G::EARLY || G::EARLY2) epi.template prefetch<ER, G::BN, G::NT>(pre, m0, n0, M, N);
 
   f32x16 acc[G::TM][G::TN];
 #pragma unroll
@@ -661,7 +680,8 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   float* Cs = reinterpret_cast<float*>(smem);
 #pragma unroll
   for (int part = 0; part < G::BM / ER; ++part) {
-    if (part > 0 || !G::EARLY) epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
+    if (part > 0 || !(G::EARLY || G::EARLY2))
+      epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
     __syncthreads();  // ring (or the previous pass's rows) no longer read
 #pragma unroll
     for (int i = 0; i < G::TM; ++i) {
@@ -783,6 +803,16 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
     return rotate_keys<T>(kv_out ? kv_out : kv, kd, n_layers, M, key_rope, false, 1.0f, s);
   }
   EpiExpand<T> e{kv, ks, bias, sigma, mode, keep, kv_out, ks_out};
+  if constexpr (sizeof(T) == 2) {
+    const int64_t wide = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+    const int64_t tiles128 = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+    const double fill128 = tiles128 <= 256 ? round_fill(tiles128, 256) : round_fill(tiles128, 512);
+    // the expansion's epilogue (the stale-cache read-modify-write) gains less
+    // from the wide tile than the bias epilogues: about 5% at equal fill
+    constexpr double kExpandWideGain = 1.05;
+    if (kExpandWideGain * round_fill(wide, 256) >= fill128)
+      return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4, true>>(A, lda, B, K, M, N, K, e, s);
+  }
   return launch<T>(A, lda, B, K, M, N, K, e, s);
 }
 
