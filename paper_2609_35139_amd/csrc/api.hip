@@ -3,6 +3,7 @@
 #include "../../include/cacherepair.h"
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <mutex>
@@ -66,25 +67,34 @@ cr_status check_dims(const cr_dims* d, const cr_kv_layout* l) {
   return CR_OK;
 }
 
-// Injective index map: with dims sorted by stride, each stride must exceed the
-// largest offset reachable through the dims inside it.
+// Injective index map over (stride, extent) pairs: with the dims sorted by
+// stride, each stride must exceed the largest offset reachable through the
+// dims inside it.  The largest offset must also stay below 2^62 elements, so
+// that no element offset a kernel forms in int64 can overflow.
+struct Dim { int64_t s, e; };
+cr_status check_injective(std::vector<Dim> dims) {
+  std::sort(dims.begin(), dims.end(), [](const Dim& a, const Dim& b) { return a.s < b.s; });
+  int64_t reach = 0;  // largest offset reachable by the dims visited so far
+  for (const Dim& x : dims) {
+    if (x.s <= reach) return CR_ERR_LAYOUT;
+    int64_t span;
+    if (__builtin_mul_overflow(x.s, x.e - 1, &span) || __builtin_add_overflow(reach, span, &reach) ||
+        reach >= ((int64_t)1 << 62))
+      return CR_ERR_LAYOUT;
+  }
+  return CR_OK;
+}
+
 cr_status check_layout(const cr_kv_layout* l, int64_t n_tokens) {
   const int64_t st[4] = {l->stride_layer, l->stride_kv, l->stride_token, l->stride_head};
   const int64_t ext[4] = {l->n_layers, 2, n_tokens, l->n_kv_heads};
-  struct D { int64_t s, e; };
-  std::vector<D> dims{{1, l->head_dim}};
+  std::vector<Dim> dims{{1, l->head_dim}};
   for (int i = 0; i < 4; ++i) {
     if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
     if (ext[i] > 1) dims.push_back({st[i], ext[i]});
   }
   if (n_tokens == 0) return CR_OK;  // no element is addressed
-  std::sort(dims.begin(), dims.end(), [](const D& a, const D& b) { return a.s < b.s; });
-  int64_t reach = 0;  // largest offset reachable by the dims visited so far
-  for (const D& x : dims) {
-    if (x.s <= reach) return CR_ERR_LAYOUT;
-    reach += x.s * (x.e - 1);
-  }
-  return CR_OK;
+  return check_injective(std::move(dims));
 }
 
 // Injectivity of a paged layout over (layer, kv, block, row, head, dim) and
@@ -96,18 +106,13 @@ cr_status check_pages(const cr_kv_layout* l, const cr_kv_pages* pg, int64_t n_to
   const int64_t st[5] = {l->stride_layer, l->stride_kv, pg->stride_block, l->stride_token,
                          l->stride_head};
   const int64_t ext[5] = {l->n_layers, 2, pg->n_blocks, bs, l->n_kv_heads};
-  struct D { int64_t s, e; };
-  std::vector<D> dims{{1, l->head_dim}};
+  std::vector<Dim> dims{{1, l->head_dim}};
   for (int i = 0; i < 5; ++i) {
     if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
     if (ext[i] > 1) dims.push_back({st[i], ext[i]});
   }
-  std::sort(dims.begin(), dims.end(), [](const D& a, const D& b) { return a.s < b.s; });
-  int64_t reach = 0;
-  for (const D& x : dims) {
-    if (x.s <= reach) return CR_ERR_LAYOUT;
-    reach += x.s * (x.e - 1);
-  }
+  const cr_status inj = check_injective(std::move(dims));
+  if (inj != CR_OK) return inj;
   const int64_t nb = (n_tokens + bs - 1) / bs;
   if (nb == 0) return CR_OK;
   if (!pg->block_table) return CR_ERR_NULL;
@@ -177,14 +182,15 @@ cr_status check_positions(const int32_t* off, int32_t n_chunks, const int32_t* r
 }
 
 cr_status check_device() {
-  static int ok[64] = {0};  // 0 unknown, 1 gfx950, -1 not
+  static std::atomic<int> ok[64];  // per device: 0 unknown, 1 gfx950, -1 not
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) return CR_ERR_DEVICE;
-  if (dev < 64 && ok[dev]) return ok[dev] > 0 ? CR_OK : CR_ERR_DEVICE;
+  const int known = dev < 64 ? ok[dev].load(std::memory_order_relaxed) : 0;
+  if (known) return known > 0 ? CR_OK : CR_ERR_DEVICE;
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return CR_ERR_DEVICE;
   const bool good = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-  if (dev < 64) ok[dev] = good ? 1 : -1;
+  if (dev < 64) ok[dev].store(good ? 1 : -1, std::memory_order_relaxed);
   return good ? CR_OK : CR_ERR_DEVICE;
 }
 

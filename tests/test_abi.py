@@ -137,6 +137,16 @@ def test_bad_layouts():
     small_head = _layout(W0)
     small_head.head_dim = 48
     assert _call_repair(W0, layout=small_head) == "CR_ERR_DIMS"
+    # a stride whose span over the layers overflows int64 (and would wrap to
+    # an offset the injectivity check accepts) is rejected, as is any layout
+    # whose largest element offset reaches 2^62
+    huge = _layout(W0)
+    huge.stride_layer = 1 << 62
+    assert _call_repair(W0, layout=huge) == "CR_ERR_LAYOUT"
+    far = _layout(W0)
+    need = -(-(1 << 62) // (t.n_layers - 1))      # (n_layers - 1) * stride >= 2^62
+    far.stride_layer = -(-need // 8) * 8
+    assert _call_repair(W0, layout=far) == "CR_ERR_LAYOUT"
 
 
 def test_workspace_and_prepared_checks():
