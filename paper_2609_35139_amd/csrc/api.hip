@@ -327,7 +327,7 @@ struct Profiler {
   std::vector<hipEvent_t> ev;        // 2 per launch slot
   std::vector<std::string> cls;      // class of each used slot
   int used = 0;
-  bool on = false;
+  std::atomic<bool> on{false};       // read without the lock on every launch
 };
 Profiler& prof() {
   static Profiler p;
@@ -631,6 +631,7 @@ cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layout, int
   if (!dims || !layout || !name || !offset_bytes || !row_stride) return CR_ERR_NULL;
   const cr_status st = check_dims(dims, layout);
   if (st != CR_OK) return st;
+  if (n_tokens < 0 || n_tokens >= ((int64_t)1 << 31) - 256) return CR_ERR_DIMS;
   const Workspace w = workspace_layout(dims, layout, n_tokens);
   if (!std::strcmp(name, "s")) { *offset_bytes = w.st; *row_stride = w.ldst; }
   else if (!std::strcmp(name, "h")) { *offset_bytes = w.h; *row_stride = dims->d_b; }

@@ -185,6 +185,9 @@ def test_workspace_views():
     assert off_s % 256 == 0 and off_h % 256 == 0 and off_s != off_h
     with pytest.raises(B.CrError):
         B.cr_workspace_view(_dims(W0), _layout(W0), 64, "nope")
+    with pytest.raises(B.CrError) as e:
+        B.cr_workspace_view(_dims(W0), _layout(W0), -1, "s")
+    assert e.value.name == "CR_ERR_DIMS"
 
 
 # ------------------------------------------------------------- variants
