@@ -705,6 +705,10 @@ template <typename T, typename G, typename Epi>
 static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N,
                                int K, const Epi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
+  // the main loop streams whole 128-byte K slabs with 16-byte copies
+  if (K <= 0 || K % G::BK != 0 || lda % G::VEC != 0 || ldb % G::VEC != 0 ||
+      reinterpret_cast<uintptr_t>(A) % 16 != 0 || reinterpret_cast<uintptr_t>(B) % 16 != 0)
+    return hipErrorInvalidValue;
   const int64_t tiles = (int64_t)((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM);
   if (tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   dim3 grid((unsigned)tiles);
