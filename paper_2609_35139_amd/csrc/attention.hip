@@ -92,31 +92,28 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   constexpr int DT = D / 32;             // 32-row tiles of O^T
   constexpr int PS = 32 / KSTEP;         // P fragments per 32-key sub-tile
   __shared__ __align__(1024) char lds[C::LDS];
-  __shared__ int red[2][4];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2, gw = wave & 3;
   const int g = lane >> 5, ql = lane & 31;
   const int head = blockIdx.x % n_heads;
   const int qt = n_qtiles - 1 - blockIdx.x / n_heads;   // latest (longest) tiles first
   const int q = qt * C::BQ + gw * 32 + ql;
   const bool qvalid = q < N;
-  const int lo = qvalid ? lo_arr[q] : 0;
-  const int hi = qvalid ? hi_arr[q] : 0;
   char* ring = lds + grp * C::RING_BYTES;
 
-  // key range of the workgroup and mask-free window of this wave's queries
-  {
-    const int wlo = wave_min(qvalid ? lo : INT_MAX);
-    const int whi = wave_max(qvalid ? hi : 0);
-    if (lane == 0 && grp == 0) { red[0][gw] = wlo; red[1][gw] = whi; }
-  }
-  const int wmax_lo = wave_max(qvalid ? lo : INT_MIN);
-  const int wmin_hi = wave_min(qvalid ? hi : INT_MAX);
-  const int mlo = qvalid ? lo : INT_MIN, mhi = qvalid ? hi : INT_MAX;
-  __syncthreads();
-  const int kv_begin = min(min(red[0][0], red[0][1]), min(red[0][2], red[0][3]));
-  const int kv_end = max(max(red[1][0], red[1][1]), max(red[1][2], red[1][3]));
+  // Rows are tokens in order and lo, hi never decrease with the row (each is
+  // the start or end of the row's request or chunk, or the row + 1), so the
+  // workgroup's key range [lo(first row), hi(last row)) and the window that
+  // every row of a wave admits, [lo(its last row), hi(its first row)), are
+  // read from the end rows: uniform loads, no reductions, no barrier.
+  const int q0 = qt * C::BQ, q1 = min(q0 + C::BQ, N) - 1;
+  const int w0 = q0 + gw * 32, w1 = min(w0 + 32, N) - 1;
+  const int kv_begin = lo_arr[q0], kv_end = hi_arr[q1];
+  const int wmax_lo = w0 < N ? lo_arr[w1] : INT_MIN;
+  const int wmin_hi = w0 < N ? hi_arr[w0] : INT_MAX;
+  const int mlo = qvalid ? lo_arr[q] : INT_MIN, mhi = qvalid ? hi_arr[q] : INT_MAX;
   const int kb = (kv_begin / C::BKV) * C::BKV;
   const int ntiles = (kv_end - kb + C::BKV - 1) / C::BKV;
   const int iters = (ntiles + 1) / 2;                  // tiles per group (group 1 may idle last)

@@ -81,6 +81,9 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
 
 // ---- flash attention over per-row key intervals [lo, hi); q pre-scaled by
 // log2(e)/sqrt(d_head); k and vt padded to n_pad >= roundup(N, 64) keys.
+// lo and hi must not decrease with the row (chunk_schedule's intervals, for
+// every topology, satisfy this): the kernel reads a tile's key range from
+// its first and last rows.
 template <typename T>
 hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, int n_heads,
                      int d_head, int64_t n_pad, const int* lo, const int* hi, hipStream_t s);
