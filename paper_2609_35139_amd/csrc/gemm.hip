@@ -250,39 +250,65 @@ struct EpiQKVh {
   struct Pre {};
   template <int ROWS, int COLS, int NT>
   __device__ void prefetch(Pre<ROWS, COLS, NT>&, int, int, int, int) const {}
+  // A 192-column tile holds 192 / (3 d_head) heads, so whatever d_head (32 or
+  // 64) it has 16 eight-column segments of Q and K and 64 columns of V: every
+  // thread's items are known at compile time.  Each pass loads the rows'
+  // positions, then every (cos, sin) entry and bias it needs, and only then
+  // computes: two load latencies per pass instead of one chain per item.
   template <int ROWS, int COLS, int LDC, int NT>
   __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>&, int m0, int n0, int M,
                       int N) const {
+    static_assert(COLS == 192, "head-interleaved 192-column tiles");
+    constexpr int QK_SEGS = COLS / 12;                  // 8-column Q and K segments per row
+    constexpr int QK_ITEMS = ROWS * QK_SEGS / NT;       // per thread
+    constexpr int V_COLS = COLS / 3;
+    constexpr int V_ITEMS = V_COLS * (ROWS / 8) / NT;
+    static_assert(NT % QK_SEGS == 0 && QK_ITEMS * NT == ROWS * QK_SEGS, "Q/K items");
+    static_assert(NT % V_COLS == 0 && V_ITEMS * NT == V_COLS * (ROWS / 8), "V items");
     const int g3 = 3 * d_head, half = d_head / 2;
-    const int groups = COLS / g3;                       // heads in the tile
-    // Q and K: 8-column segments, both members of every rotate-half pair
-    const int qk_segs = groups * (2 * d_head / 8);
     const float qsc = 1.4426950408889634f / __builtin_sqrtf((float)d_head);
-    for (int idx = threadIdx.x; idx < ROWS * qk_segs; idx += NT) {
-      const int r = idx / qk_segs, sg = idx % qk_segs;
-      const int grp = sg / (2 * d_head / 8), w = (sg % (2 * d_head / 8)) * 8;  // w in [0, 2 d_head)
-      const int part = w / d_head, i = w % d_head;
-      const int c = grp * g3 + w;                       // tile column
-      const int hh = (n0 + c) / g3;
-      const bool is_q = part == 0;
+    // Q and K: a thread keeps one segment (threadIdx % QK_SEGS) over rows
+    // threadIdx / QK_SEGS + j * NT / QK_SEGS; both members of every
+    // rotate-half pair are read from the staged tile
+    const int sg = threadIdx.x % QK_SEGS;
+    const int grp = sg / (2 * d_head / 8), w = (sg % (2 * d_head / 8)) * 8;  // w in [0, 2 d_head)
+    const int part = w / d_head, i = w % d_head;
+    const int c = grp * g3 + w;                         // tile column
+    const int hh = (n0 + c) / g3;
+    const bool is_q = part == 0, first = i < half;
+    const int pi = first ? i + half : i - half;         // partner index in the head
+    const int fi = first ? i : i - half;
+    const bool col_ok = n0 + c < N;
+    const int row_end = is_q ? M : (int)n_pad;
+    int p[QK_ITEMS];
+#pragma unroll
+    for (int j = 0; j < QK_ITEMS; ++j) {
+      const int gm = m0 + threadIdx.x / QK_SEGS + j * (NT / QK_SEGS);
+      p[j] = gm < M ? pos[gm] : 0;
+    }
+    float bx[8], by[8];
+    const int bcol = part * d_b + hh * d_head;
+    if (col_ok) { load8f(bias + bcol + i, bx); load8f(bias + bcol + pi, by); }
+    float4 t4[QK_ITEMS][4];
+#pragma unroll
+    for (int j = 0; j < QK_ITEMS; ++j) {
+      const float4* src = reinterpret_cast<const float4*>(rope + (int64_t)p[j] * half + fi);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t4[j][e] = src[e];
+    }
+    const float osc = is_q ? qsc : 1.0f;
+#pragma unroll
+    for (int j = 0; j < QK_ITEMS; ++j) {
+      const int r = threadIdx.x / QK_SEGS + j * (NT / QK_SEGS);
       const int gm = m0 + r;
-      if (gm >= (is_q ? M : (int)n_pad) || n0 + c >= N) continue;
-      const bool first = i < half;
-      const int pi = first ? i + half : i - half;       // partner index in the head
-      const int fi = first ? i : i - half;
-      float x[8], y[8], bx[8], by[8];
+      if (gm >= row_end || !col_ok) continue;
+      float x[8], y[8];
       load8f(Cs + r * LDC + c, x);
       load8f(Cs + r * LDC + c - i + pi, y);
-      const int bcol = part * d_b + hh * d_head;
-      load8f(bias + bcol + i, bx);
-      load8f(bias + bcol + pi, by);
-      const int p = gm < M ? pos[gm] : 0;
-      const float4* t4 = reinterpret_cast<const float4*>(rope + (int64_t)p * half + fi);
-      const float osc = is_q ? qsc : 1.0f;
       float v[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float4 t = t4[e];   // (cos, sin) of pairs 2e and 2e+1
+        const float4 t = t4[j][e];   // (cos, sin) of pairs 2e and 2e+1
         const float x0 = x[2 * e] + bx[2 * e], y0 = y[2 * e] + by[2 * e];
         const float x1 = x[2 * e + 1] + bx[2 * e + 1], y1 = y[2 * e + 1] + by[2 * e + 1];
         v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
@@ -291,22 +317,25 @@ struct EpiQKVh {
       Vec8<T> o; o.from_float(v);
       o.store((is_q ? q : k) + (int64_t)gm * d_b + hh * d_head + i);
     }
-    // V: transposed, vt[head][d][token], 8 tokens per 16-byte store;
-    // consecutive threads take consecutive columns (conflict-free LDS reads)
-    const int v_cols = groups * d_head;
-    for (int idx = threadIdx.x; idx < v_cols * (ROWS / 8); idx += NT) {
-      const int vc = idx % v_cols, r = (idx / v_cols) * 8;
-      const int grp = vc / d_head, i = vc % d_head;
-      const int c = grp * g3 + 2 * d_head + i;
-      const int gn = n0 + c, gm = m0 + r;
-      if (gn >= N || gm + 8 > n_pad) continue;
-      const int hh = gn / g3;
-      const float bb = bias[2 * d_b + hh * d_head + i];
+    // V: transposed, vt[head][d][token], 8 tokens per 16-byte store; a thread
+    // keeps one column (consecutive threads take consecutive columns, so the
+    // LDS reads are conflict-free)
+    const int vc = threadIdx.x % V_COLS;
+    const int vgrp = vc / d_head, vi = vc % d_head;
+    const int vcol = vgrp * g3 + 2 * d_head + vi;
+    const int vgn = n0 + vcol;
+    if (vgn >= N) return;
+    const int vh = vgn / g3;
+    const float bb = bias[2 * d_b + vh * d_head + vi];
+#pragma unroll
+    for (int j = 0; j < V_ITEMS; ++j) {
+      const int r = (threadIdx.x / V_COLS + j * (NT / V_COLS)) * 8, gm = m0 + r;
+      if (gm + 8 > n_pad) continue;
       float v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + c] + bb;
+      for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + vcol] + bb;
       Vec8<T> o; o.from_float(v);
-      o.store(vt + (int64_t)(hh * d_head + i) * n_pad + gm);
+      o.store(vt + (int64_t)(vh * d_head + vi) * n_pad + gm);
     }
   }
 };
