@@ -58,6 +58,26 @@ def test_masks_match_their_definitions(mask, lengths):
 
 @pytest.mark.parametrize("mask", O.MASKS)
 @pytest.mark.parametrize("lengths", LENGTHS)
+def test_allowed_keys_are_intervals_whose_ends_never_decrease(mask, lengths):
+    """Under every topology, row i's keys are one interval [lo_i, hi_i) that
+    holds i, and lo and hi never decrease with i.  The attention kernel
+    relies on this: it reads a query tile's key range from its first and
+    last rows."""
+    w = small_workload(lengths)
+    c = O.token_chunk_ids(w.chunk_offsets)
+    r = O.token_request_ids(w.chunk_offsets, w.request_chunks)
+    allowed = O.attention_allowed(mask, c, r)
+    n = len(c)
+    lo = np.array([np.flatnonzero(row)[0] for row in allowed])
+    hi = np.array([np.flatnonzero(row)[-1] + 1 for row in allowed])
+    for i in range(n):
+        assert allowed[i, lo[i]:hi[i]].all() and allowed[i].sum() == hi[i] - lo[i]
+    assert (lo <= np.arange(n)).all() and (np.arange(n) < hi).all()
+    assert (np.diff(lo) >= 0).all() and (np.diff(hi) >= 0).all()
+
+
+@pytest.mark.parametrize("mask", O.MASKS)
+@pytest.mark.parametrize("lengths", LENGTHS)
 def test_chunkwise_attention_equals_explicit_mask_for_every_topology(mask, lengths):
     w = small_workload(lengths)
     n = w.n_tokens
