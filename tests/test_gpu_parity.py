@@ -69,6 +69,9 @@ SMALL = [
          n_heads=4, d_seg=8),
     dict(lengths=((128, 1), (77,)), dtype="bf16", L=1, H=1, dh=224, E=64, d_c=128, d_b=128,
          n_heads=2, d_seg=24),
+    # bf16 attention over 32-wide heads, query tiles spanning chunks
+    dict(lengths=((150, 0, 97), (33, 170)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
+         d_b=128, n_heads=4, d_seg=8),
 ]
 
 
@@ -147,6 +150,31 @@ def test_parity_ragged_batch_prefix_sampled():
     # later chunks of every request were repaired too
     last = W.kv_layer_major_to_canonical(kv[:, :, -64:].float().cpu().numpy())
     assert np.abs(last - W.kv_layer_major_to_canonical(inp.kv[:, :, -64:])).max() > 0
+
+
+@pytest.mark.timeout(600)
+def test_parity_head_interleaved_qkv_with_32_wide_heads_first_chunk():
+    """4,096 tokens with d_b = 1024 in 32 heads of 32: the QKV projection takes
+    the 256x192 tiles of whole heads (six heads per tile) and the attention
+    its 32-wide kernel.  The whole batch is repaired in one call; every token
+    of the first chunk is checked against the oracle run on that chunk."""
+    import torch
+    w = small_workload(((512,) * 8,), dtype="bf16", L=2, H=2, dh=128, E=256, d_seg=24,
+                       d_c=256, d_b=1024, n_blocks=2, n_heads=32, ffn_mult=4, vocab=1000)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    kv = to_device(w, inp.kv)
+    emb = to_device(w, inp.token_embeds)
+    rep.repair(kv, w.chunk_offsets, w.request_chunks, emb)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(kv).all())
+    idx, off, req = truncate_requests(w, keep_chunks=1)
+    Yg = W.kv_layer_major_to_canonical(
+        kv[:, :, torch.from_numpy(idx).cuda()].float().cpu().numpy())
+    X = W.kv_layer_major_to_canonical(inp.kv[:, :, idx])
+    ref = O.repair(X, inp.token_embeds[idx], off, req, inp.weights, w.target.head_dim,
+                   w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps)
+    assert_parity(Yg, ref, X, w)
 
 
 # ------------------------------------------------------------ invariants
