@@ -72,6 +72,9 @@ SMALL = [
     # bf16 attention over 32-wide heads, query tiles spanning chunks
     dict(lengths=((150, 0, 97), (33, 170)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
          d_b=128, n_heads=4, d_seg=8),
+    # the widest backbone accepted (d_b = 2048): LayerNorm rows of 2048
+    dict(lengths=((130, 70),), dtype="bf16", L=1, H=1, dh=64, E=64, d_c=64, d_b=2048,
+         n_heads=32, d_seg=8),
 ]
 
 
