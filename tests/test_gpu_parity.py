@@ -75,6 +75,11 @@ SMALL = [
     # the widest backbone accepted (d_b = 2048): LayerNorm rows of 2048
     dict(lengths=((130, 70),), dtype="bf16", L=1, H=1, dh=64, E=64, d_c=64, d_b=2048,
          n_heads=32, d_seg=8),
+    # no repair blocks: fused features straight into the final LayerNorm and head
+    dict(lengths=((70, 0, 133), (5, 61)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
+         d_b=128, n_heads=2, d_seg=8, n_blocks=0),
+    dict(lengths=((40, 97),), dtype="f32", L=2, H=1, dh=64, E=64, d_c=64, d_b=128,
+         n_heads=4, d_seg=8, n_blocks=0),
 ]
 
 
