@@ -80,6 +80,9 @@ SMALL = [
          d_b=128, n_heads=2, d_seg=8, n_blocks=0),
     dict(lengths=((40, 97),), dtype="f32", L=2, H=1, dh=64, E=64, d_c=64, d_b=128,
          n_heads=4, d_seg=8, n_blocks=0),
+    # one token per chunk (block-causal = token-causal): every key tile masked
+    dict(lengths=((1,) * 150, (1,) * 20), dtype="bf16", L=1, H=2, dh=64, E=64, d_c=64,
+         d_b=128, n_heads=2, d_seg=8),
 ]
 
 
