@@ -201,6 +201,9 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
       issue(it + C::STAGES - 1, ((J + C::STAGES - 1) % C::STAGES) * C::STAGE_BYTES);
     if (it >= mine) return;         // group 1 without a last tile: only keeps the barrier count
     constexpr int SO = J * C::STAGE_BYTES;
+    // the compiler's interleaving of LDS reads with MFMAs for this tile's
+    // fragment reads and score products (-2% per launch, same results)
+    __builtin_amdgcn_iglp_opt(0);
 
     // S^T = K Q^T for two 32-key sub-tiles; all fragment reads first
     frag kf[2][QF];
