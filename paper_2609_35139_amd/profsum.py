@@ -58,7 +58,7 @@ def bench_line(path):
 
 def short_name(n):
     n = re.sub(r"\(.*", "", n)
-    for k in ("EpiBias", "EpiQKVh", "EpiExpandRope", "EpiExpand"):
+    for k in ("EpiBias", "EpiQKVh", "EpiQKV", "EpiExpandRope", "EpiExpand"):
         if k in n:
             return "gemm_nt_kernel<" + k + ">"
     m = re.search(r"cr::(\w+)|_ZN2cr\d+(\w+?)I|_ZN2cr\d+(\w+)E", n)
