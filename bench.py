@@ -26,7 +26,10 @@ FUNCTION_OF = {
     "gemm_compress": "gemm_nt_kernel<EpiBias>", "gemm_token": "gemm_nt_kernel<EpiBias>",
     "gemm_fuse": "gemm_nt_kernel<EpiBias>", "gemm_inject": "gemm_nt_kernel<EpiBias>",
     "gemm_oproj": "gemm_nt_kernel<EpiBias>", "gemm_ffn1": "gemm_nt_kernel<EpiBias>",
-    "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKVh>",
+    # the QKV projection runs on 256x192 tiles of whole heads (EpiQKVh) or on
+    # 128x128 tiles in the weights' column order (EpiQKV), whichever fills
+    # the grid's rounds better for the workload
+    "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKVh|EpiQKV>",
     "gemm_expand": "gemm_nt_kernel<EpiExpand>", "attention": "attention_kernel",
     "layernorm": "layernorm_kernel", "compress_segments": "compress_segments_kernel",
     "schedule": "schedule_kernel", "rope_table": "rope_table_kernel",
