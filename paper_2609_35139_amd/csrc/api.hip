@@ -350,10 +350,10 @@ hipError_t timed(const char* name, hipStream_t s, F&& f) {
   LaunchEvents& le = launch_events();
   le.start = P.ev[2 * slot];
   le.stop = P.ev[2 * slot + 1];
-  const hipError_t e = f();
+  hipError_t e = f();
   if (le.start) {   // the stage launched nothing: an empty interval
-    hipEventRecord(P.ev[2 * slot], s);
-    hipEventRecord(P.ev[2 * slot + 1], s);
+    if (e == hipSuccess) e = hipEventRecord(P.ev[2 * slot], s);
+    if (e == hipSuccess) e = hipEventRecord(P.ev[2 * slot + 1], s);
   }
   le = LaunchEvents{};
   return e;
@@ -856,9 +856,10 @@ cr_status cr_pipeline_create(cr_pipeline* pipeline) {
 
 cr_status cr_pipeline_destroy(cr_pipeline p) {
   if (!p) return CR_ERR_NULL;
+  // teardown: a failed destroy leaves nothing the caller could act on
   for (int i = 0; i < 2; ++i) {
-    if (p->copied[i]) hipEventDestroy(p->copied[i]);
-    if (p->done[i]) hipEventDestroy(p->done[i]);
+    if (p->copied[i]) (void)hipEventDestroy(p->copied[i]);
+    if (p->done[i]) (void)hipEventDestroy(p->done[i]);
   }
   delete p;
   return CR_OK;
@@ -1041,7 +1042,7 @@ cr_status cr_profile_enable(int32_t max_launches) {
   if (max_launches < 0) return CR_ERR_DIMS;
   Profiler& P = prof();
   std::lock_guard<std::mutex> g(P.mu);
-  for (hipEvent_t e : P.ev) hipEventDestroy(e);
+  for (hipEvent_t e : P.ev) (void)hipEventDestroy(e);   // teardown of the previous slots
   P.ev.clear();
   P.cls.clear();
   P.used = 0;
