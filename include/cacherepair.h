@@ -430,8 +430,11 @@ CR_API cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layo
  * max_launches = 0 disables profiling and destroys them.  Launches beyond
  * max_launches since the last reset are not timed.  cr_profile_read waits for
  * the recorded events, then fills up to max_stats entries, one per kernel
- * class in first-launch order, and resets the record.  This is process-wide
- * state guarded by a mutex; profile one stream at a time.
+ * class in first-launch order, and resets the record (also when it returns
+ * an error).  A stage whose launch failed is left out of the record: its
+ * events were never recorded.  This is process-wide state guarded by a
+ * mutex, held while a timed stage is enqueued (so cr_profile_enable waits
+ * for it); profile one stream at a time.
  */
 typedef struct {
     char name[32];        /* kernel class, e.g. "attention", "gemm_ffn1" */

@@ -72,10 +72,18 @@ cr_status check_dims(const cr_dims* d, const cr_kv_layout* l) {
 // dims inside it.  The largest offset must also stay below 2^62 elements, so
 // that no element offset a kernel forms in int64 can overflow.
 struct Dim { int64_t s, e; };
-cr_status check_injective(std::vector<Dim> dims) {
-  std::sort(dims.begin(), dims.end(), [](const Dim& a, const Dim& b) { return a.s < b.s; });
+// At most six (stride, extent) pairs: dim, head, token, (block,) K/V, layer.
+// Fixed capacity, so validating a call allocates nothing.
+struct Dims {
+  Dim d[6];
+  int n = 0;
+  void push_back(Dim x) { d[n++] = x; }
+};
+cr_status check_injective(Dims dims) {
+  std::sort(dims.d, dims.d + dims.n, [](const Dim& a, const Dim& b) { return a.s < b.s; });
   int64_t reach = 0;  // largest offset reachable by the dims visited so far
-  for (const Dim& x : dims) {
+  for (int i = 0; i < dims.n; ++i) {
+    const Dim& x = dims.d[i];
     if (x.s <= reach) return CR_ERR_LAYOUT;
     int64_t span;
     if (__builtin_mul_overflow(x.s, x.e - 1, &span) || __builtin_add_overflow(reach, span, &reach) ||
@@ -88,13 +96,14 @@ cr_status check_injective(std::vector<Dim> dims) {
 cr_status check_layout(const cr_kv_layout* l, int64_t n_tokens) {
   const int64_t st[4] = {l->stride_layer, l->stride_kv, l->stride_token, l->stride_head};
   const int64_t ext[4] = {l->n_layers, 2, n_tokens, l->n_kv_heads};
-  std::vector<Dim> dims{{1, l->head_dim}};
+  Dims dims;
+  dims.push_back({1, l->head_dim});
   for (int i = 0; i < 4; ++i) {
     if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
     if (ext[i] > 1) dims.push_back({st[i], ext[i]});
   }
   if (n_tokens == 0) return CR_OK;  // no element is addressed
-  return check_injective(std::move(dims));
+  return check_injective(dims);
 }
 
 // Injectivity of a paged layout over (layer, kv, block, row, head, dim) and
@@ -106,12 +115,13 @@ cr_status check_pages(const cr_kv_layout* l, const cr_kv_pages* pg, int64_t n_to
   const int64_t st[5] = {l->stride_layer, l->stride_kv, pg->stride_block, l->stride_token,
                          l->stride_head};
   const int64_t ext[5] = {l->n_layers, 2, pg->n_blocks, bs, l->n_kv_heads};
-  std::vector<Dim> dims{{1, l->head_dim}};
+  Dims dims;
+  dims.push_back({1, l->head_dim});
   for (int i = 0; i < 5; ++i) {
     if (st[i] < 0 || st[i] % 8 != 0) return CR_ERR_LAYOUT;
     if (ext[i] > 1) dims.push_back({st[i], ext[i]});
   }
-  const cr_status inj = check_injective(std::move(dims));
+  const cr_status inj = check_injective(dims);
   if (inj != CR_OK) return inj;
   const int64_t nb = (n_tokens + bs - 1) / bs;
   if (nb == 0) return CR_OK;
@@ -244,13 +254,21 @@ struct BlockP {
 // Prepared (device-optimised) weights: matrices [out][in] in the storage
 // dtype, vectors fp32.  The reinjection projections of all blocks are stacked
 // into one [B*d_b][d_c] matrix so that P_b(s) is computed for every block by
-// a single GEMM.
+// a single GEMM.  The blocks' tensors follow one another with the same
+// layout, so block b's offsets are block 0's plus b times the block stride.
 struct Prepared {
   int64_t kc, kc_pad;
   uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_tok, b_tok, w_fuse, b_fuse;
   uint64_t w_inj, b_inj;
-  std::vector<BlockP> blk;
+  BlockP blk0;
+  uint64_t blk_stride;
   uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta, total;
+  BlockP blk(int b) const {
+    const uint64_t o = (uint64_t)b * blk_stride;
+    const BlockP& q = blk0;
+    return BlockP{q.ln1_g + o, q.ln1_b + o, q.w_qkv + o, q.b_qkv + o, q.w_o + o, q.b_o + o,
+                  q.ln2_g + o, q.ln2_b + o, q.w_ff1 + o, q.b_ff1 + o, q.w_ff2 + o, q.b_ff2 + o};
+  }
 };
 
 Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
@@ -268,6 +286,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
   p.w_tok = a.take(db * E * T); p.b_tok = a.take(db * F);
   p.w_fuse = a.take(db * (dc + db) * T); p.b_fuse = a.take(db * F);
   p.w_inj = a.take(d->n_blocks * db * dc * T); p.b_inj = a.take(d->n_blocks * db * F);
+  const uint64_t first = a.off;
   for (int b = 0; b < d->n_blocks; ++b) {
     BlockP q;
     q.ln1_g = a.take(db * F); q.ln1_b = a.take(db * F);
@@ -276,8 +295,12 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
     q.ln2_g = a.take(db * F); q.ln2_b = a.take(db * F);
     q.w_ff1 = a.take(r * db * db * T); q.b_ff1 = a.take(r * db * F);
     q.w_ff2 = a.take(db * r * db * T); q.b_ff2 = a.take(db * F);
-    p.blk.push_back(q);
+    if (b == 0) {
+      p.blk0 = q;
+      p.blk_stride = a.off - first;
+    }
   }
+  if (d->n_blocks == 0) p.blk_stride = 0;
   p.ln_f_g = a.take(db * F); p.ln_f_b = a.take(db * F);
   p.w_out = a.take(D * db * T); p.b_out = a.take(D * F); p.sigma_delta = a.take(D * F);
   p.total = a.off;
@@ -326,6 +349,7 @@ struct Profiler {
   std::mutex mu;
   std::vector<hipEvent_t> ev;        // 2 per launch slot
   std::vector<std::string> cls;      // class of each used slot
+  std::vector<char> valid;           // the slot's events were recorded
   int used = 0;
   std::atomic<bool> on{false};       // read without the lock on every launch
 };
@@ -335,27 +359,32 @@ Profiler& prof() {
 }
 
 // Launch `f` on stream s, bracketed by events when profiling is enabled.
+// While a slot is in use the profiler's lock is held, so a concurrent
+// cr_profile_enable cannot destroy its events; a stage that fails leaves its
+// slot marked invalid (its events may never be recorded).
 template <typename F>
 hipError_t timed(const char* name, hipStream_t s, F&& f) {
   Profiler& P = prof();
-  int slot = -1;
-  if (P.on) {
-    std::lock_guard<std::mutex> g(P.mu);
-    if (P.on && P.used < (int)P.ev.size() / 2) {
-      slot = P.used++;
-      P.cls.emplace_back(name);
-    }
+  if (!P.on) return f();
+  std::unique_lock<std::mutex> g(P.mu);
+  if (!P.on || P.used >= (int)P.ev.size() / 2) {
+    g.unlock();
+    return f();
   }
-  if (slot < 0) return f();
+  const int slot = P.used++;
+  P.cls.emplace_back(name);
+  P.valid.push_back(0);
+  const hipEvent_t e0 = P.ev[2 * slot], e1 = P.ev[2 * slot + 1];
   LaunchEvents& le = launch_events();
-  le.start = P.ev[2 * slot];
-  le.stop = P.ev[2 * slot + 1];
+  le.start = e0;
+  le.stop = e1;
   hipError_t e = f();
-  if (le.start) {   // the stage launched nothing: an empty interval
-    if (e == hipSuccess) e = hipEventRecord(P.ev[2 * slot], s);
-    if (e == hipSuccess) e = hipEventRecord(P.ev[2 * slot + 1], s);
+  if (e == hipSuccess && le.start) {   // the stage launched nothing: an empty interval
+    e = hipEventRecord(e0, s);
+    if (e == hipSuccess) e = hipEventRecord(e1, s);
   }
   le = LaunchEvents{};
+  P.valid[slot] = e == hipSuccess;
   return e;
 }
 
@@ -404,7 +433,7 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
   CR_TRY(vec("b_fuse", p.b_fuse, db));
   for (int b = 0; b < d->n_blocks; ++b) {
     const std::string q = "blk" + std::to_string(b) + ".";
-    const BlockP& B = p.blk[b];
+    const BlockP B = p.blk(b);
     CR_TRY(mat(q + "w_inj", p.w_inj + (uint64_t)b * db * dc * sizeof(T), dc, db, dc));
     CR_TRY(vec(q + "b_inj", p.b_inj + (uint64_t)b * db * 4, db));
     CR_TRY(vec(q + "ln1_g", B.ln1_g, db));
@@ -532,7 +561,7 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
                           rj ? inj : nullptr, ldinj, false, s); }));
   // h holds x_b = h^{b-1} + P_b(s) on entry to block b, h^B after the last block
   for (int b = 0; b < B; ++b) {
-    const BlockP& Bk = P.blk[b];
+    const BlockP Bk = P.blk(b);
     const T* next_inj = rj && b + 1 < B ? inj + (int64_t)(b + 1) * db : nullptr;
     CR_TRY(timed("layernorm", s, [&] {
         return cr::layernorm<T>(h, db, a, db, PF(Bk.ln1_g), PF(Bk.ln1_b), M, db, eps, s); }));
@@ -1045,12 +1074,19 @@ cr_status cr_profile_enable(int32_t max_launches) {
   for (hipEvent_t e : P.ev) (void)hipEventDestroy(e);   // teardown of the previous slots
   P.ev.clear();
   P.cls.clear();
+  P.valid.clear();
   P.used = 0;
   P.on = false;
   if (max_launches == 0) return CR_OK;
-  P.ev.resize(2 * (size_t)max_launches);
-  for (hipEvent_t& e : P.ev)
-    if (hipEventCreate(&e) != hipSuccess) return CR_ERR_DEVICE;
+  P.ev.resize(2 * (size_t)max_launches, nullptr);
+  for (hipEvent_t& e : P.ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (hipEvent_t& x : P.ev)
+        if (x) (void)hipEventDestroy(x);   // teardown of a partial set
+      P.ev.clear();
+      return CR_ERR_DEVICE;
+    }
+  }
   P.on = true;
   return CR_OK;
 }
@@ -1062,17 +1098,25 @@ cr_status cr_profile_read(cr_kernel_stat* stats, int32_t max_stats, int32_t* n_s
   std::vector<std::string> names;
   std::vector<int> launches;
   std::vector<double> total;
-  for (int i = 0; i < P.used; ++i) {
-    if (hipEventSynchronize(P.ev[2 * i + 1]) != hipSuccess) return CR_ERR_LAUNCH;
+  cr_status st = CR_OK;
+  for (int i = 0; i < P.used && st == CR_OK; ++i) {
+    if (!P.valid[i]) continue;        // its stage failed: nothing was timed
     float ms = 0.f;
-    if (hipEventElapsedTime(&ms, P.ev[2 * i], P.ev[2 * i + 1]) != hipSuccess) return CR_ERR_LAUNCH;
+    if (hipEventSynchronize(P.ev[2 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, P.ev[2 * i], P.ev[2 * i + 1]) != hipSuccess) {
+      st = CR_ERR_LAUNCH;
+      break;
+    }
     size_t k = std::find(names.begin(), names.end(), P.cls[i]) - names.begin();
     if (k == names.size()) { names.push_back(P.cls[i]); launches.push_back(0); total.push_back(0); }
     launches[k] += 1;
     total[k] += ms;
   }
+  // the slots are free again whatever happened
   P.used = 0;
   P.cls.clear();
+  P.valid.clear();
+  if (st != CR_OK) return st;
   *n_stats = (int32_t)names.size();
   if (!stats) return CR_OK;
   if (max_stats < (int32_t)names.size()) return CR_ERR_CAPACITY;

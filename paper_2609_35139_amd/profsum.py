@@ -1,6 +1,6 @@
 """Text summaries of rocprofv3 output for the repair kernels.
 
-Two kinds of summary are written (short text files, a few KB):
+Three kinds of summary are written (short text files, a few KB):
 
 * ``kernel_stats``: the ``--kernel-trace --stats`` table of one command, with
   the bench line of the same run appended;
@@ -9,13 +9,23 @@ Two kinds of summary are written (short text files, a few KB):
   by the factor the same counter reads for a device-to-device copy of known
   size in the same process.  The file records a hash of the sources that
   build the kernel, so a reader can tell whether the counters still describe
-  the current code.
+  the current code;
+* ``counters``: per kernel class, the means over its dispatches of one
+  ``--pmc`` pass of SQ counters, and the ratios derived from them: MFMA-pipe
+  busy time over CU-busy time (SQ_VALU_MFMA_BUSY_CYCLES counts one cycle per
+  1,024 MFMA FLOPs of one SIMD, so it is divided by four SIMDs times
+  SQ_BUSY_CU_CYCLES, the busy cycles summed over the CUs), MFMA FLOPs per
+  launch (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512), the share of wave cycles spent
+  waiting on any dependency, VALU-active cycles per wave cycle, and LDS bank
+  conflict cycles per LDS-active cycle.
 
 Usage::
 
     python -m paper_2609_35139_amd.profsum stats <kernel_stats.csv> <bench.json> <out.txt> <command...>
     python -m paper_2609_35139_amd.profsum traffic <fetch_counter_collection.csv> \
         <write_counter_collection.csv> <bench.json> <class> <out.txt> <command...>
+    python -m paper_2609_35139_amd.profsum counters <counter_collection.csv> <bench.json> \
+        <out.txt> <command...>
 """
 import csv
 import hashlib
@@ -38,6 +48,8 @@ CLASS_KERNEL = {
 for _c in ("gemm_compress", "gemm_token", "gemm_fuse", "gemm_inject", "gemm_oproj", "gemm_ffn1",
            "gemm_ffn2"):
     CLASS_KERNEL[_c] = ("EpiBias", ["gemm.hip", "common.h", "launch.h"])
+# the bench's 8192^3 bf16 library GEMM (measured-peak reference; no sources here)
+CLASS_KERNEL["library_gemm_8192"] = ("Cijk_", [])
 
 
 def source_hash(cls):
@@ -180,6 +192,63 @@ def traffic(fetch_csv, write_csv, bench_json, cls, command):
     return "\n".join(out) + "\n"
 
 
+SQ_RATIOS = (
+    ("mfma_busy_of_cu_busy", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", 4.0),
+    ("wait_of_wave_cycles", "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES", 1.0),
+    ("valu_active_of_wave_cycles", "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES", 1.0),
+    ("lds_conflict_of_lds_active", "SQ_LDS_BANK_CONFLICT", "SQ_ACTIVE_INST_LDS", 1.0),
+)
+
+
+def counters(csv_path, bench_json, command, n_cus=256):
+    """Per-class means of one --pmc pass (one row per dispatch and counter)
+    and the derived ratios of SQ_RATIOS."""
+    b = bench_line(bench_json)
+    disp = {}
+    for r in csv.DictReader(open(csv_path)):
+        d = int(r["Dispatch_Id"])
+        e = disp.setdefault(d, {"name": r["Kernel_Name"],
+                                "dur_ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    per_step = {k["class"]: k["launches_per_step"] for k in b["kernels"]}
+    seq = gemm_sequence(per_step.get("gemm_oproj", 0))
+    by_cls, k = {}, 0
+    for d in sorted(disp):
+        e = disp[d]
+        cls = None
+        for c, (sub, _) in CLASS_KERNEL.items():
+            if sub != "EpiBias" and sub in e["name"] and "EpiExpandRope" not in e["name"]:
+                cls = c
+        if "EpiBias" in e["name"]:
+            cls = seq[k % len(seq)]
+            k += 1
+        if cls:
+            by_cls.setdefault(cls, []).append(e)
+    names = sorted({n for e in disp.values() for n in e if n.isupper() or n.startswith("SQ_")})
+    out = [f"# SQ counters per kernel class, workload {b['config']['workload']}",
+           f"# command: {command}",
+           "# means over the class's dispatches of the profiled run; duration from the",
+           "# dispatch timestamps of the same (serialised) run",
+           f"# mfma_busy_of_cu_busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 * SQ_BUSY_CU_CYCLES); "
+           f"SQ_BUSY_CU_CYCLES / {n_cus} / duration = mean CU-busy cycles per ns",
+           ""]
+    for cls in [c for c in CLASS_KERNEL if c in by_cls]:
+        es = by_cls[cls]
+        mean = {n: sum(e.get(n, 0.0) for e in es) / len(es) for n in names}
+        dur = sum(e["dur_ns"] for e in es) / len(es)
+        out.append(f"[{cls}] dispatches {len(es)}, duration_us {dur / 1e3:.2f}")
+        for n in names:
+            out.append(f"  {n}: {mean[n]:.6g}")
+        if mean.get("SQ_INSTS_VALU_MFMA_MOPS_BF16"):
+            out.append(f"  mfma_flops_per_launch: {mean['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.6g}")
+        if mean.get("SQ_BUSY_CU_CYCLES"):
+            out.append(f"  cu_busy_cycles_per_ns: {mean['SQ_BUSY_CU_CYCLES'] / n_cus / dur:.3f}")
+        for label, num, den, f in SQ_RATIOS:
+            if mean.get(den):
+                out.append(f"  {label}: {mean.get(num, 0.0) / (f * mean[den]):.4f}")
+    return "\n".join(out) + "\n"
+
+
 def read_traffic(path, cls):
     """Traffic bytes per launch recorded for cls, or None when the file is
     missing or the kernel sources changed since the counters were taken."""
@@ -203,6 +272,9 @@ def main(argv):
     elif mode == "traffic":
         fetch_csv, write_csv, bench_json, cls, out = argv[1:6]
         text = traffic(fetch_csv, write_csv, bench_json, cls, " ".join(argv[6:]))
+    elif mode == "counters":
+        csv_path, bench_json, out = argv[1:4]
+        text = counters(csv_path, bench_json, " ".join(argv[4:]))
     else:
         raise SystemExit(__doc__)
     with open(out, "w") as fh:

@@ -1,11 +1,13 @@
 """Paged cache layout (block table) on the GPU: the repair, its variants and
-cr_rotate_keys read and write the blocks in place and give results
-bit-identical to the contiguous layer-major cache."""
+cr_rotate_keys read and write the blocks in place, match the fp64 oracle
+with the same options, and give results bit-identical to the contiguous
+layer-major cache."""
 import numpy as np
 import pytest
 
+import oracle as O
 import workloads as W
-from helpers import repairer_for, small_workload, to_device
+from helpers import assert_parity, oracle_kwargs, oracle_repair, repairer_for, small_workload, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -78,7 +80,12 @@ def test_paged_repair_is_bit_identical(case, opts):
     torch.cuda.synchronize()
     got = kv_p.float().cpu().numpy()
     ref = kv_a.float().cpu().numpy()
-    assert np.array_equal(_gather(got, table, w.n_tokens, bs), ref)
+    gathered = _gather(got, table, w.n_tokens, bs)
+    # against the oracle with the same options, then against the contiguous run
+    assert_parity(W.kv_layer_major_to_canonical(gathered),
+                  oracle_repair(inp, **oracle_kwargs(w, **extra_opts)),
+                  W.kv_layer_major_to_canonical(inp.kv), w)
+    assert np.array_equal(gathered, ref)
     # blocks outside the table and rows past the last token are untouched
     used = np.zeros(got.shape[:4], bool)
     for tok in range(w.n_tokens):
@@ -106,5 +113,14 @@ def test_paged_rotate_keys_is_bit_identical():
                     pages=dict(block_size=bs, n_blocks=pool.shape[2], stride_block=sB,
                                block_table=table))
     torch.cuda.synchronize()
-    assert np.array_equal(_gather(kv_p.float().cpu().numpy(), table, w.n_tokens, bs),
-                          kv_a.float().cpu().numpy())
+    gathered = _gather(kv_p.float().cpu().numpy(), table, w.n_tokens, bs)
+    # against the oracle's rotation (one rounding of the stored result plus
+    # fp32 arithmetic on the pair), then against the contiguous run
+    X = W.kv_layer_major_to_canonical(inp.kv).astype(np.float64)
+    pos = O.positions(w.chunk_offsets, w.request_chunks) + np.array([3, 40])[
+        O.token_request_ids(w.chunk_offsets, w.request_chunks)]
+    f = 5e5 ** (-2.0 * np.arange(t.head_dim // 2) / t.head_dim)
+    ref = O.rotate_keys(X, pos, f, t.n_layers, t.n_kv_heads, t.head_dim)
+    got = W.kv_layer_major_to_canonical(gathered)
+    assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 4e-6 * np.abs(X).max())
+    assert np.array_equal(gathered, kv_a.float().cpu().numpy())

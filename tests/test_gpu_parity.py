@@ -136,31 +136,49 @@ def test_parity_workload_full_large(i):
     assert_parity(Y, oracle_repair(inp), W.kv_layer_major_to_canonical(inp.kv), w)
 
 
-@pytest.mark.timeout(900)
-def test_parity_ragged_batch_prefix_sampled():
+@pytest.fixture(scope="module")
+def ragged_repaired():
     """Ragged packed batch (4 requests x 16 chunks, 31,503 tokens) repaired in
-    one call at full size; every token of the first two chunks of each request
-    is checked against the oracle run on exactly those chunks (by the
-    block-causal mask they see nothing else)."""
+    one call at full size, in the launch configuration the bench times; the
+    repaired cache stays on the device."""
     import torch
     w = W.WORKLOADS[4]
+    print(f"[ragged] generating {w.name}: {w.n_tokens} tokens", flush=True)
     inp = W.make_inputs(w)
     rep = repairer_for(w, inp.weights)
     kv = to_device(w, inp.kv)
     emb = to_device(w, inp.token_embeds)
+    print("[ragged] repairing on the GPU", flush=True)
     rep.repair(kv, w.chunk_offsets, w.request_chunks, emb)
     torch.cuda.synchronize()
-    assert bool(torch.isfinite(kv).all())
-    idx, off, req = truncate_requests(w, keep_chunks=2)
-    Yg = W.kv_layer_major_to_canonical(
-        kv[:, :, torch.from_numpy(idx).cuda()].float().cpu().numpy())
-    X = W.kv_layer_major_to_canonical(inp.kv[:, :, idx])
-    ref = O.repair(X, inp.token_embeds[idx], off, req, inp.weights, w.target.head_dim,
-                   w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps)
-    assert_parity(Yg, ref, X, w)
-    # later chunks of every request were repaired too
-    last = W.kv_layer_major_to_canonical(kv[:, :, -64:].float().cpu().numpy())
-    assert np.abs(last - W.kv_layer_major_to_canonical(inp.kv[:, :, -64:])).max() > 0
+    del emb, rep
+    return w, inp, kv
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("r", range(4))
+def test_parity_ragged_batch_full(ragged_repaired, r):
+    """Every token of request r of the ragged batch (all 16 chunks, including
+    the query tiles that straddle request boundaries in the packed call) and
+    every cache coordinate against the fp64 oracle run on that request alone
+    (requests never attend to each other), head applied one layer's columns
+    at a time so host memory stays bounded."""
+    from helpers import SlabParity, oracle_request_slabs
+    w, inp, kv = ragged_repaired
+    t = w.target
+    off, rc = w.chunk_offsets, w.request_chunks
+    t0, t1 = int(off[rc[r]]), int(off[rc[r + 1]])
+    acc = SlabParity(w)
+    width = 2 * t.n_kv_heads * t.head_dim
+    for c0, Xc, Yr in oracle_request_slabs(inp, r):
+        layer = c0 // width
+        Yg = kv[layer, :, t0:t1].float().cpu().numpy()          # [2, n, H, dh]
+        Yg = np.ascontiguousarray(Yg.transpose(1, 0, 2, 3)).reshape(t1 - t0, width)
+        acc.add(Yg, Yr, Xc, c0)
+        if layer % 8 == 7:
+            print(f"[ragged] request {r}: layers 0..{layer} compared", flush=True)
+    assert acc.rows == t1 - t0
+    acc.check()
 
 
 @pytest.mark.timeout(600)

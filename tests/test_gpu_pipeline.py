@@ -1,5 +1,6 @@
 """Out-of-place repair and the pipelined host -> device -> repair path on the
-GPU.  Both write the same values as the in-place repair of the same request:
+GPU.  Both match the fp64 oracle with the same options, and write the same
+values as the in-place repair of the same request:
 the out-of-place epilogue stores the repaired coordinates into a second cache
 (and copies the coordinates the variant leaves alone), the pipeline copies
 each request from pinned host memory into a staging slot and repairs it into
@@ -7,8 +8,10 @@ its destination while the next request is in flight."""
 import numpy as np
 import pytest
 
+import oracle as O
 import workloads as W
-from helpers import repairer_for, small_workload, to_device
+from helpers import (assert_parity, oracle_kwargs, oracle_repair, repairer_for, small_workload,
+                     to_device)
 from test_gpu_paged import _gather, _pool
 
 pytestmark = pytest.mark.gpu
@@ -60,6 +63,9 @@ def test_out_of_place_matches_in_place(dtype, variant):
                options=B.Options(kv_out=out.data_ptr(), layout_out=rep.layout(w.n_tokens),
                                  **opts))
     torch.cuda.synchronize()
+    X = W.kv_layer_major_to_canonical(inp.kv)
+    assert_parity(W.kv_layer_major_to_canonical(out.float().cpu().numpy()),
+                  oracle_repair(inp, **oracle_kwargs(w, **opts)), X, w)
     assert torch.equal(out, kv_a)
     assert torch.equal(kv_in, before)
 
@@ -77,6 +83,8 @@ def test_out_of_place_paged(direction):
     kv_a = to_device(w, inp.kv)
     rep.repair(kv_a, w.chunk_offsets, w.request_chunks, emb, options=B.Options(apply="v"))
     ref = kv_a.float().cpu().numpy()
+    Y_or = oracle_repair(inp, apply="v")
+    X = W.kv_layer_major_to_canonical(inp.kv)
     pool, table = _pool(w, inp.kv.astype(np.float32), bs, 3, 29)
     lay_p, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, pool.shape[2], bs,
                                B.CR_DTYPE_BF16)
@@ -90,7 +98,9 @@ def test_out_of_place_paged(direction):
                                      pages_out=pages))
         torch.cuda.synchronize()
         got = out.float().cpu().numpy()
-        assert np.array_equal(_gather(got, table, w.n_tokens, bs), ref)
+        gathered = _gather(got, table, w.n_tokens, bs)
+        assert_parity(W.kv_layer_major_to_canonical(gathered), Y_or, X, w)
+        assert np.array_equal(gathered, ref)
         used = np.zeros(got.shape[:4], bool)
         for tok in range(w.n_tokens):
             used[:, :, table[tok // bs], tok % bs] = True
@@ -104,6 +114,7 @@ def test_out_of_place_paged(direction):
                    options=B.Options(apply="v", pages=pages, kv_out=out.data_ptr(),
                                      layout_out=rep.layout(w.n_tokens)))
         torch.cuda.synchronize()
+        assert_parity(W.kv_layer_major_to_canonical(out.float().cpu().numpy()), Y_or, X, w)
         assert np.array_equal(out.float().cpu().numpy(), ref)
         assert torch.equal(kv_p, before)
 
@@ -118,6 +129,23 @@ def _requests(w, inp):
         out.append((np.ascontiguousarray(inp.kv[:, :, t0:t1]),
                     np.ascontiguousarray(inp.token_embeds[t0:t1]), local))
     return out
+
+
+def _check_request_against_oracle(w, inp, r, out, opts, pos_offset):
+    """Request r's destination cache (layer-major [L][2][n][H][dh]) against the
+    fp64 oracle run on that request alone."""
+    off, rc = w.chunk_offsets, w.request_chunks
+    t0, t1 = off[rc[r]], off[rc[r + 1]]
+    if t1 == t0:
+        return
+    local = np.asarray(off[rc[r]:rc[r + 1] + 1], np.int64) - t0
+    X = W.kv_layer_major_to_canonical(inp.kv[:, :, t0:t1])
+    kw = oracle_kwargs(w, **dict(opts, position_offset=[pos_offset])) if opts else {}
+    if kw:
+        kw["n_kv_heads"] = w.target.n_kv_heads
+    ref = O.repair(X, inp.token_embeds[t0:t1], local.astype(np.int32), None, inp.weights,
+                   w.target.head_dim, w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps, **kw)
+    assert_parity(W.kv_layer_major_to_canonical(out.float().cpu().numpy()), ref, X, w)
 
 
 def _pinned(w, arr):
@@ -162,6 +190,8 @@ def test_pipeline_matches_direct_repair(dtype, placed):
         comp_s.synchronize()
         copy_s.synchronize()
         for r in range(len(reqs)):
+            if rnd == 0:
+                _check_request_against_oracle(w, inp, r, outs[r], opts, 11 * r)
             assert torch.equal(outs[r], refs[r]), (rnd, r)
 
 
@@ -204,7 +234,10 @@ def test_pipeline_into_paged_pool():
         rep.repair(kv_d, off_r, [0, len(off_r) - 1], to_device(w, emb_r))
         torch.cuda.synchronize()
         n = off_r[-1]
-        assert np.array_equal(_gather(got, tables[r], n, bs), kv_d.float().cpu().numpy()), r
+        gathered = _gather(got, tables[r], n, bs)
+        import torch as _t
+        _check_request_against_oracle(w, inp, r, _t.from_numpy(gathered), {}, 0)
+        assert np.array_equal(gathered, kv_d.float().cpu().numpy()), r
         for tok in range(n):
             used[:, :, tables[r][tok // bs], tok % bs] = True
     assert np.all(got[~used] == SENTINEL)

@@ -408,3 +408,62 @@ def test_whole_network_matches_brute_force():
     Yb = _brute_repair(inp)
     X = W.kv_layer_major_to_canonical(inp.kv)
     assert np.max(np.abs(Y - Yb)) <= 1e-11 * np.max(np.abs(Y - X))
+
+
+@pytest.mark.parametrize("case", ["ragged", "tiny"])
+def test_request_by_request_slabbed_oracle_equals_whole_batch(case):
+    """The memory-bounded way the large packed batch is checked (each request
+    on its own, the head one column slab at a time) gives the whole-batch
+    oracle's values to rounding: requests never see each other and the head
+    is a per-column map."""
+    from helpers import SlabParity, oracle_request_slabs
+    if case == "ragged":
+        w = small_workload(((30, 0, 17), (5, 41), (9,)), L=3, H=2, dh=16, E=32, d_c=16,
+                           d_b=32, n_heads=2, d_seg=4)
+    else:
+        w = W.WORKLOADS[0]
+    inp = W.make_inputs(w)
+    Y = oracle_repair(inp)
+    X = W.kv_layer_major_to_canonical(inp.kv)
+    off, rc = w.chunk_offsets, w.request_chunks
+    acc = SlabParity(w)
+    for r in range(len(rc) - 1):
+        t0, t1 = off[rc[r]], off[rc[r + 1]]
+        for c0, Xc, Yr in oracle_request_slabs(inp, r, layers_per_slab=1):
+            c1 = c0 + Xc.shape[1]
+            assert np.array_equal(Xc, X[t0:t1, c0:c1])
+            assert np.abs(Yr - Y[t0:t1, c0:c1]).max() <= 1e-12 * np.abs(Y).max()
+            acc.add(Yr, Y[t0:t1, c0:c1], X[t0:t1, c0:c1], c0)
+    assert acc.rows == w.n_tokens
+    assert acc.report()["max_abs"] <= 1e-12 * np.abs(Y).max()
+
+
+def test_slab_parity_matches_whole_array_statistics_and_catches_a_dropped_slab():
+    """SlabParity's accumulated statistics equal parity_report's on the whole
+    arrays, and a zeroed V slab (the failure the per-slab gate exists for)
+    fails its check (at a repairer width where the residual is well above
+    bf16 rounding, as in the real workloads)."""
+    from helpers import SlabParity, parity_report
+    w = small_workload(((20, 12),), L=2, H=2, dh=8, E=32, d_c=64, d_b=512, n_heads=8,
+                       dtype="bf16")
+    inp = W.make_inputs(w)
+    Y = oracle_repair(inp)
+    X = W.kv_layer_major_to_canonical(inp.kv)
+    rng = np.random.default_rng(0)
+    Yg = Y + rng.normal(0, 1e-3, Y.shape)
+    acc = SlabParity(w)
+    slab = 2 * 8 * 2
+    for c0 in range(0, Y.shape[1], slab):
+        for rows in (slice(0, 13), slice(13, None)):
+            acc.add(Yg[rows, c0:c0 + slab], Y[rows, c0:c0 + slab], X[rows, c0:c0 + slab], c0)
+    full = parity_report(Yg, Y, X, w)
+    got = acc.report()
+    for k in ("max_abs", "global_rel", "worst_slab_rel", "resid_rel"):
+        assert got[k] == pytest.approx(full[k], rel=1e-12)
+    acc.check()
+    bad = Yg.copy()
+    bad[:, 16:32] = X[:, 16:32]          # layer 0's V residual dropped
+    acc2 = SlabParity(w)
+    acc2.add(bad, Y, X, 0)
+    with pytest.raises(AssertionError):
+        acc2.check()
