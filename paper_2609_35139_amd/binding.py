@@ -31,7 +31,9 @@ EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_b
            "cr_prepare_weights", "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair",
            "cr_default_options", "cr_repair_ex", "cr_rotate_workspace_bytes", "cr_rotate_keys",
            "cr_pipeline_create", "cr_pipeline_destroy", "cr_pipeline_staging_bytes",
-           "cr_repair_pipelined", "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]
+           "cr_repair_pipelined", "cr_workspace_view", "cr_profile_enable", "cr_profile_read",
+           "cr_repair_static"]
+CR_STATIC_SCRATCH_BYTES = 192 << 20
 CR_MASK = {"block_causal": 0, "token_causal": 1, "bidirectional": 2, "block_diagonal": 3}
 CR_APPLY = {"kv": 0, "k": 1, "v": 2}
 
@@ -118,6 +120,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cr_default_options.restype = None
     lib.cr_default_options.argtypes = [P(cr_options)]
     lib.cr_repair_ex.argtypes = lib.cr_repair.argtypes + [P(cr_options)]
+    lib.cr_repair_static.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
+                                     c_int32, c_void_p, P(cr_dims), c_void_p, c_uint64, c_void_p]
     lib.cr_rotate_workspace_bytes.argtypes = [P(cr_kv_layout), c_int64, P(c_uint64)]
     lib.cr_rotate_keys.argtypes = [c_void_p, P(cr_kv_layout), P(c_int32), c_int32, P(c_int32),
                                    c_int32, P(cr_rope), P(c_int32), c_int32, P(cr_kv_pages),
@@ -137,7 +141,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                  "cr_workspace_bytes", "cr_chunk_schedule", "cr_repair", "cr_repair_ex",
                  "cr_rotate_workspace_bytes", "cr_rotate_keys", "cr_pipeline_create",
                  "cr_pipeline_destroy", "cr_pipeline_staging_bytes", "cr_repair_pipelined",
-                 "cr_workspace_view", "cr_profile_enable", "cr_profile_read"]:
+                 "cr_workspace_view", "cr_profile_enable", "cr_profile_read", "cr_repair_static"]:
         getattr(lib, name).restype = c_int32
     _lib = lib
     return lib
@@ -222,6 +226,17 @@ def cr_repair(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
         req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r,
         token_embeds, ctypes.byref(dims), prepared, prepared_bytes, workspace, workspace_bytes,
         stream), "cr_repair")
+
+
+def cr_repair_static(kv: int, layout: cr_kv_layout, chunk_offsets: Sequence[int],
+                     request_chunks: Optional[Sequence[int]], token_embeds: int, dims: cr_dims,
+                     prepared: int, prepared_bytes: int, stream: Optional[int] = None) -> None:
+    off, m = _i32(chunk_offsets)
+    req, r = _i32(request_chunks)
+    _check(load().cr_repair_static(
+        kv, ctypes.byref(layout), off.ctypes.data_as(POINTER(c_int32)), m,
+        req.ctypes.data_as(POINTER(c_int32)) if req is not None else None, r,
+        token_embeds, ctypes.byref(dims), prepared, prepared_bytes, stream), "cr_repair_static")
 
 
 class Options:

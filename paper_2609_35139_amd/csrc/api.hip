@@ -741,12 +741,15 @@ bool same_shape(const cr_kv_layout* a, const cr_kv_layout* b) {
 }
 
 // Host-side validation of one cr_repair_ex call (nothing is enqueued).
+// static_ws: the workspace is the library's static scratch (workspace is
+// null here; workspace_bytes is the scratch size).
 cr_status validate_call(const void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
                         int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
                         const void* token_embeds, const cr_dims* dims, const void* prepared,
                         uint64_t prepared_bytes, const void* workspace, uint64_t workspace_bytes,
-                        const cr_options& o, Call* c) {
-  if (!kv || !layout || !token_embeds || !dims || !prepared || !workspace) return CR_ERR_NULL;
+                        const cr_options& o, Call* c, bool static_ws = false) {
+  if (!kv || !layout || !token_embeds || !dims || !prepared || (!workspace && !static_ws))
+    return CR_ERR_NULL;
   cr_status st = check_dims(dims, layout);
   if (st != CR_OK) return st;
   st = check_offsets(chunk_offsets, n_chunks, request_chunks, n_requests);
@@ -794,7 +797,8 @@ cr_status validate_call(const void* kv, const cr_kv_layout* layout, const int32_
   }
   if (prepared_bytes < prepared_layout(dims, layout).total || !aligned(prepared, ALIGN))
     return CR_ERR_WORKSPACE;
-  if (workspace_bytes < workspace_layout(dims, layout, N).total || !aligned(workspace, ALIGN))
+  if (workspace_bytes < workspace_layout(dims, layout, N).total ||
+      (!static_ws && !aligned(workspace, ALIGN)))
     return CR_ERR_WORKSPACE;
   c->N = N;
   int max_len = 0;
@@ -837,6 +841,35 @@ Staging staging_layout(const cr_dims* d, const cr_kv_layout* l, int64_t max_toke
   g.emb_bytes = align_up((uint64_t)max_tokens * d->d_model * T);
   g.slot_bytes = g.kv_bytes + g.emb_bytes;
   return g;
+}
+
+}  // namespace
+
+// Workspace of cr_repair_static: a device array of the library.  Every GPU
+// that loads the library holds its own copy until the process ends.  Host
+// code never uses this name as an address (on the host it only stands for
+// the symbol): each device's copy is found once through hipGetSymbolAddress
+// with that device current, and that address is what the kernels receive.
+static __device__ __align__(256) char scratch[CR_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+// This GPU's address of the scratch array, looked up on the first call made
+// with the device current and kept per device.
+cr_status scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return CR_ERR_DEVICE;
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CR_ERR_DEVICE;
+    if (!aligned(p, ALIGN)) return CR_ERR_DEVICE;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return CR_OK;
 }
 
 }  // namespace
@@ -993,6 +1026,27 @@ cr_status cr_repair(void* kv, const cr_kv_layout* layout, const int32_t* chunk_o
   return cr_repair_ex(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
                       token_embeds, dims, prepared, prepared_bytes, workspace, workspace_bytes,
                       stream, &o);
+}
+
+cr_status cr_repair_static(void* kv, const cr_kv_layout* layout, const int32_t* chunk_offsets,
+                           int32_t n_chunks, const int32_t* request_chunks, int32_t n_requests,
+                           const void* token_embeds, const cr_dims* dims, const void* prepared,
+                           uint64_t prepared_bytes, void* stream) {
+  cr_options o;
+  cr_default_options(&o);
+  Call c;
+  cr_status st = validate_call(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
+                               token_embeds, dims, prepared, prepared_bytes, nullptr,
+                               CR_STATIC_SCRATCH_BYTES, o, &c, /*static_ws=*/true);
+  if (st != CR_OK) return st;
+  if (c.N == 0) return CR_OK;
+  st = check_device();
+  if (st != CR_OK) return st;
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != CR_OK) return st;
+  return enqueue_call(kv, layout, chunk_offsets, n_chunks, request_chunks, n_requests,
+                      token_embeds, dims, prepared, ws, c, reinterpret_cast<hipStream_t>(stream));
 }
 
 // workspace of cr_rotate_keys: lo, hi, pos, gpos, block table (int32 each)

@@ -365,3 +365,22 @@ def test_pipeline_validation():
     bad.n_layers += 1
     assert _call_pipeline(w, [dict(item, layout_out=bad)]) == "CR_ERR_LAYOUT"
     assert _call_pipeline(w, [dict(item, chunk_offsets=[0, 30, 20])]) == "CR_ERR_OFFSETS"
+
+
+def test_static_scratch_entry_point_validates_on_the_host():
+    """cr_repair_static rejects a NULL cache and a workspace need beyond
+    CR_STATIC_SCRATCH_BYTES before touching any device."""
+    w = W.WORKLOADS[3]                     # 10 x 512 Llama-3-8B-shaped: needs > 192 MiB
+    dims, lay = _dims(w), _layout(w)
+    assert B.cr_workspace_bytes(dims, lay, w.n_tokens) > B.CR_STATIC_SCRATCH_BYTES
+    prep_bytes = B.cr_prepared_bytes(dims, lay)
+    with pytest.raises(B.CrError) as e:
+        B.cr_repair_static(0x10000, lay, w.chunk_offsets, w.request_chunks, 0x20000, dims,
+                           0x30000, prep_bytes, None)
+    assert e.value.name == "CR_ERR_WORKSPACE"
+    with pytest.raises(B.CrError) as e:
+        B.cr_repair_static(0, lay, w.chunk_offsets, w.request_chunks, 0x20000, dims, 0x30000,
+                           prep_bytes, None)
+    assert e.value.name == "CR_ERR_NULL"
+    w2 = W.WORKLOADS[2]                    # the headline request fits
+    assert B.cr_workspace_bytes(_dims(w2), _layout(w2), w2.n_tokens) <= B.CR_STATIC_SCRATCH_BYTES
