@@ -30,10 +30,20 @@
  *    completion is observed through the stream.
  *  - Every validation happens before anything is enqueued: on an error return
  *    no device memory has been touched.
- *  - The caller owns every buffer.  The library allocates no device memory.
+ *  - The caller owns every buffer.  No call allocates device memory (the one
+ *    static device array, cr_repair_static's workspace, is created when the
+ *    library's code is loaded on a device).
  *  - Storage dtype (bf16 or fp32) is a property of the cache layout and applies
  *    to the cache, the token embeddings, the canonical weight blob and all
- *    intermediate activations; accumulation is always fp32.
+ *    intermediate activations; accumulation is always fp32.  It is a runtime
+ *    field of cr_kv_layout, not a build-time choice: one library holds both
+ *    the bf16 path and the fp32 debug path, so one process can compare them,
+ *    and no "which dtype was this built for" query exists.
+ *  - Weights reach the repair calls as the prepared buffer that
+ *    cr_prepare_weights builds once from the canonical blob (matrices
+ *    transposed to [out][in], 1/sigma_stale folded in, vectors widened to
+ *    fp32), so no call converts weights; the canonical blob described by
+ *    cr_weights_layout stays the one interchange format.
  *  - No exceptions cross the ABI.  Entry points are reentrant given distinct
  *    workspaces.
  */

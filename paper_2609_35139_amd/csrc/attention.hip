@@ -22,10 +22,10 @@
 // softmax keeps a per-row reference max that is not a running max: the
 // score accumulators start at minus the reference, and the exact tile max is
 // taken (with a rescale of the output accumulators) only for a row's first
-// keys or when a tile's probability sum exceeds 2^24.  Softmax is invariant
-// to the reference, so this changes rounding only, and per score the VALU
-// does an exp2, half a pack and half a dot2 instead of also a max and a
-// subtraction.
+// keys or when a tile's probability sum exceeds 2^24, a choice made row by
+// row.  Softmax is invariant to the reference, so this changes rounding
+// only, and per score the VALU does an exp2, half a pack and half a dot2
+// instead of also a max and a subtraction.
 #include <climits>
 #include <type_traits>
 
@@ -274,14 +274,16 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     // Fast path: the reference max stays where it is.  A probability is at
     // most its lane's tile sum, so a sum <= kMaxTileSum rules out overflow
     // (O and l accumulate in fp32 with ample range).  Otherwise, and for a
-    // row without a reference yet, the wave takes the exact row max, rescales
-    // its accumulators and recomputes the tile's probabilities.
-    bool exact = __any(m_ref == -INFINITY);
+    // row without a reference yet, the row takes the exact row max, rescales
+    // its accumulators and recomputes the tile's probabilities.  The choice
+    // is made per query row (its two lanes agree through one exchange), so
+    // no row's rounding depends on the scores of another row.  The fast
+    // probabilities are skipped only when every row of the wave takes the
+    // exact path anyway.
     float ts = 0.f;
-    if (!exact) {
-      ts = probs(std::false_type{}, 0.f);
-      exact = __any(!(ts <= kMaxTileSum));
-    }
+    if (!__all(m_ref == -INFINITY)) ts = probs(std::false_type{}, 0.f);
+    int exact = m_ref == -INFINITY || !(ts <= kMaxTileSum);
+    exact |= __shfl_xor(exact, 32, WAVE);
     if (exact) {
       float mx = -INFINITY;
 #pragma unroll

@@ -292,3 +292,85 @@ def test_layouts_give_identical_results():
     assert np.array_equal(got_tm, ref)
     assert np.array_equal(got_pad, ref)
     assert torch.all(pad[..., dh:] == 0)      # padding untouched
+
+
+def _block0_scores(inp, weights, w):
+    """fp64 block-0 attention scores in exp2 units, [heads, N, N], of the
+    oracle's forward pass on this input (the kernel's score units)."""
+    taps = {}
+    X = W.kv_layer_major_to_canonical(inp.kv)
+    O.repair_features(X, inp.token_embeds, w.chunk_offsets, w.request_chunks, weights,
+                      w.target.head_dim, w.rep.n_heads, w.rep.rope_theta, w.rep.ln_eps, taps=taps)
+    Wt = lambda n: np.asarray(weights["blk0." + n], np.float64)
+    x = taps["h0"] + taps["s"] @ Wt("w_inj") + Wt("b_inj")
+    a = O.layer_norm(x, Wt("ln1_g"), Wt("ln1_b"), w.rep.ln_eps)
+    qkv = a @ Wt("w_qkv") + Wt("b_qkv")
+    n, db, nh = x.shape[0], w.rep.d_b, w.rep.n_heads
+    d = db // nh
+    pos = O.positions(w.chunk_offsets, w.request_chunks)
+    q = O.rope(qkv[:, :db].reshape(n, nh, d), pos, w.rep.rope_theta)
+    k = O.rope(qkv[:, db:2 * db].reshape(n, nh, d), pos, w.rep.rope_theta)
+    return np.einsum("ihd,jhd->hij", q, k) / np.sqrt(d) / np.log(2.0)
+
+
+def _rows_forced_exact(sc, lo, hi, margin=26.0):
+    """Rows that the kernel sends down the exact softmax path after their
+    first tile: in one of the two key-tile groups (even / odd 64-key tiles of
+    a workgroup starting at key 0), a tile's best allowed score exceeds the
+    group's reference (its first allowed tile's max) by more than `margin`
+    log2 units, i.e. the tile's probability sum exceeds 2^24."""
+    H, n, _ = sc.shape
+    ntiles = -(-n // 64)
+    rows = set()
+    for h in range(H):
+        for i in range(n):
+            for g in (0, 1):
+                ref = None
+                for t in range(g, ntiles, 2):
+                    a, b = max(64 * t, lo[i]), min(64 * t + 64, hi[i])
+                    if a >= b:
+                        continue
+                    m = sc[h, i, a:b].max()
+                    if ref is None:
+                        ref = m
+                    elif m - ref > margin:
+                        rows.add(i)
+                        ref = m
+    return rows
+
+
+def test_softmax_path_is_chosen_per_row():
+    """The attention's fast / exact softmax choice is made per query row: a
+    later chunk whose rows are forced down the exact path (block 0's Q/K
+    weights scaled by 32, so scores span far more than 24 log2 units) leaves
+    every row of the earlier chunks bit-identical, including the rows that
+    share a wave with it."""
+    # chunk starts at 140 and 200 fall inside waves (32 rows), and the later
+    # rows see at least three 64-key tiles (a second tile in one key group)
+    w = small_workload(((140, 60, 80),), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64, d_b=128,
+                       n_heads=2, d_seg=8, ffn_mult=4)
+    inp = W.make_inputs(w)
+    wts = dict(inp.weights)
+    wts["blk0.w_qkv"] = wts["blk0.w_qkv"] * np.float32(32.0)          # exact in bf16
+    rep = repairer_for(w, wts)
+    Y0 = gpu_repair(inp, weights=wts, rep=rep)
+    assert np.all(np.isfinite(Y0))
+    off = w.chunk_offsets
+    n = w.n_tokens
+    lo = np.zeros(n, np.int64)
+    hi = np.array([off[c + 1] for c in O.token_chunk_ids(off)])
+    rng = np.random.default_rng(5)
+    for k in (1, 2):
+        kv = inp.kv.copy()
+        kv[:, :, off[k]:] = W.round_to_storage(kv[:, :, off[k]:] * -1.5 + 0.25, "bf16")
+        emb = inp.token_embeds.copy()
+        emb[off[k]:] = W.round_to_storage(rng.standard_normal(emb[off[k]:].shape) * 3.0, "bf16")
+        pert = W.Inputs(w, kv, inp.token_ids, emb, wts, inp.k_scale)
+        # the perturbed later rows of the wave that straddles the chunk start
+        # are sent down the exact path
+        wave = range(off[k], min(32 * (off[k] // 32) + 32, n))
+        forced = _rows_forced_exact(_block0_scores(pert, wts, w), lo, hi)
+        assert forced & set(wave), k
+        Y1 = gpu_repair(inp, weights=wts, kv=kv, embeds=emb, rep=rep)
+        assert np.array_equal(Y0[:off[k]], Y1[:off[k]]), k
+        assert not np.array_equal(Y0[off[k]:], Y1[off[k]:])
