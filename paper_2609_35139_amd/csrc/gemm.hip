@@ -264,56 +264,93 @@ struct EpiQKVh {
     const int g3 = 3 * d_head, rem = n % g3;
     return (rem / d_head) * d_b + (n / g3) * d_head + rem % d_head;
   }
-  template <int ROWS, int COLS, int NT>
-  struct Pre {};
-  template <int ROWS, int COLS, int NT>
-  __device__ void prefetch(Pre<ROWS, COLS, NT>&, int, int, int, int) const {}
   // A 192-column tile holds 192 / (3 d_head) heads, so whatever d_head (32 or
   // 64) it has 16 eight-column segments of Q and K and 64 columns of V: every
-  // thread's items are known at compile time.  Each pass loads the rows'
-  // positions, then every (cos, sin) entry and bias it needs, and only then
-  // computes: two load latencies per pass instead of one chain per item.
-  template <int ROWS, int COLS, int LDC, int NT>
-  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>&, int m0, int n0, int M,
-                      int N) const {
+  // thread's items are known at compile time.  A thread keeps one Q/K segment
+  // (threadIdx % QK_SEGS) over rows threadIdx / QK_SEGS + j * NT / QK_SEGS,
+  // and one V column over groups of 8 rows.
+  template <int ROWS, int COLS, int NT>
+  struct Map {
     static_assert(COLS == 192, "head-interleaved 192-column tiles");
-    constexpr int QK_SEGS = COLS / 12;                  // 8-column Q and K segments per row
-    constexpr int QK_ITEMS = ROWS * QK_SEGS / NT;       // per thread
-    constexpr int V_COLS = COLS / 3;
-    constexpr int V_ITEMS = V_COLS * (ROWS / 8) / NT;
+    static constexpr int QK_SEGS = COLS / 12;                 // 8-column Q and K segments per row
+    static constexpr int QK_ITEMS = ROWS * QK_SEGS / NT;      // per thread
+    static constexpr int V_COLS = COLS / 3;
+    static constexpr int V_ITEMS = V_COLS * (ROWS / 8) / NT;
     static_assert(NT % QK_SEGS == 0 && QK_ITEMS * NT == ROWS * QK_SEGS, "Q/K items");
     static_assert(NT % V_COLS == 0 && V_ITEMS * NT == V_COLS * (ROWS / 8), "V items");
+  };
+  struct Seg {
+    int c, hh, i, pi, fi, part;
+    bool first, col_ok;
+  };
+  template <int QK_SEGS>
+  __device__ Seg seg(int n0, int N) const {
     const int g3 = 3 * d_head, half = d_head / 2;
-    const float qsc = 1.4426950408889634f / __builtin_sqrtf((float)d_head);
-    // Q and K: a thread keeps one segment (threadIdx % QK_SEGS) over rows
-    // threadIdx / QK_SEGS + j * NT / QK_SEGS; both members of every
-    // rotate-half pair are read from the staged tile
     const int sg = threadIdx.x % QK_SEGS;
     const int grp = sg / (2 * d_head / 8), w = (sg % (2 * d_head / 8)) * 8;  // w in [0, 2 d_head)
-    const int part = w / d_head, i = w % d_head;
-    const int c = grp * g3 + w;                         // tile column
-    const int hh = (n0 + c) / g3;
-    const bool is_q = part == 0, first = i < half;
-    const int pi = first ? i + half : i - half;         // partner index in the head
-    const int fi = first ? i : i - half;
-    const bool col_ok = n0 + c < N;
-    const int row_end = is_q ? M : (int)n_pad;
-    int p[QK_ITEMS];
+    Seg g;
+    g.part = w / d_head;
+    g.i = w % d_head;
+    g.c = grp * g3 + w;                                   // tile column
+    g.hh = (n0 + g.c) / g3;
+    g.first = g.i < half;
+    g.pi = g.first ? g.i + half : g.i - half;             // partner index in the head
+    g.fi = g.first ? g.i : g.i - half;
+    g.col_ok = n0 + g.c < N;
+    return g;
+  }
+  // The pass's positions, (cos, sin) entries and biases are loaded before the
+  // pass's tile is staged, so their latency hides behind the staging.
+  template <int ROWS, int COLS, int NT>
+  struct Pre {
+    float bx[8], by[8], bb;
+    float4 t4[Map<ROWS, COLS, NT>::QK_ITEMS][4];
+  };
+  // the thread's V column: tile column, head, index in the head
+  template <int V_COLS>
+  __device__ void vcol(int n0, int& col, int& vh, int& vi) const {
+    const int g3 = 3 * d_head, vc = threadIdx.x % V_COLS;
+    vi = vc % d_head;
+    col = (vc / d_head) * g3 + 2 * d_head + vi;
+    vh = (n0 + col) / g3;
+  }
+  template <int ROWS, int COLS, int NT>
+  __device__ void prefetch(Pre<ROWS, COLS, NT>& pr, int m0, int n0, int M, int N) const {
+    using MP = Map<ROWS, COLS, NT>;
+    const Seg g = seg<MP::QK_SEGS>(n0, N);
+    const int half = d_head / 2;
+    int p[MP::QK_ITEMS];
 #pragma unroll
-    for (int j = 0; j < QK_ITEMS; ++j) {
-      const int gm = m0 + threadIdx.x / QK_SEGS + j * (NT / QK_SEGS);
+    for (int j = 0; j < MP::QK_ITEMS; ++j) {
+      const int gm = m0 + threadIdx.x / MP::QK_SEGS + j * (NT / MP::QK_SEGS);
       p[j] = gm < M ? pos[gm] : 0;
     }
-    float bx[8], by[8];
-    const int bcol = part * d_b + hh * d_head;
-    if (col_ok) { load8f(bias + bcol + i, bx); load8f(bias + bcol + pi, by); }
-    float4 t4[QK_ITEMS][4];
+    const int bcol = g.part * d_b + g.hh * d_head;
+    if (g.col_ok) { load8f(bias + bcol + g.i, pr.bx); load8f(bias + bcol + g.pi, pr.by); }
 #pragma unroll
-    for (int j = 0; j < QK_ITEMS; ++j) {
-      const float4* src = reinterpret_cast<const float4*>(rope + (int64_t)p[j] * half + fi);
+    for (int j = 0; j < MP::QK_ITEMS; ++j) {
+      const float4* src = reinterpret_cast<const float4*>(rope + (int64_t)p[j] * half + g.fi);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) t4[j][e] = src[e];
+      for (int e = 0; e < 4; ++e) pr.t4[j][e] = src[e];
     }
+    int col, vh, vi;
+    vcol<MP::V_COLS>(n0, col, vh, vi);
+    if (n0 + col < N) pr.bb = bias[2 * d_b + vh * d_head + vi];
+  }
+  template <int ROWS, int COLS, int LDC, int NT>
+  __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& pr, int m0, int n0, int M,
+                      int N) const {
+    using MP = Map<ROWS, COLS, NT>;
+    constexpr int QK_SEGS = MP::QK_SEGS, QK_ITEMS = MP::QK_ITEMS;
+    constexpr int V_COLS = MP::V_COLS, V_ITEMS = MP::V_ITEMS;
+    const int g3 = 3 * d_head;
+    const float qsc = 1.4426950408889634f / __builtin_sqrtf((float)d_head);
+    const Seg g = seg<QK_SEGS>(n0, N);
+    const int c = g.c, hh = g.hh, i = g.i, pi = g.pi;
+    const bool is_q = g.part == 0, first = g.first, col_ok = g.col_ok;
+    const int row_end = is_q ? M : (int)n_pad;
+    const float* bx = pr.bx;
+    const float* by = pr.by;
     const float osc = is_q ? qsc : 1.0f;
 #pragma unroll
     for (int j = 0; j < QK_ITEMS; ++j) {
@@ -326,7 +363,7 @@ struct EpiQKVh {
       float v[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float4 t = t4[j][e];   // (cos, sin) of pairs 2e and 2e+1
+        const float4 t = pr.t4[j][e];   // (cos, sin) of pairs 2e and 2e+1
         const float x0 = x[2 * e] + bx[2 * e], y0 = y[2 * e] + by[2 * e];
         const float x1 = x[2 * e + 1] + bx[2 * e + 1], y1 = y[2 * e + 1] + by[2 * e + 1];
         v[2 * e] = (first ? x0 * t.x - y0 * t.y : x0 * t.x + y0 * t.y) * osc;
@@ -338,20 +375,17 @@ struct EpiQKVh {
     // V: transposed, vt[head][d][token], 8 tokens per 16-byte store; a thread
     // keeps one column (consecutive threads take consecutive columns, so the
     // LDS reads are conflict-free)
-    const int vc = threadIdx.x % V_COLS;
-    const int vgrp = vc / d_head, vi = vc % d_head;
-    const int vcol = vgrp * g3 + 2 * d_head + vi;
-    const int vgn = n0 + vcol;
-    if (vgn >= N) return;
-    const int vh = vgn / g3;
-    const float bb = bias[2 * d_b + vh * d_head + vi];
+    int vcl, vh, vi;
+    vcol<V_COLS>(n0, vcl, vh, vi);
+    if (n0 + vcl >= N) return;
+    const float bb = pr.bb;
 #pragma unroll
     for (int j = 0; j < V_ITEMS; ++j) {
       const int r = (threadIdx.x / V_COLS + j * (NT / V_COLS)) * 8, gm = m0 + r;
       if (gm + 8 > n_pad) continue;
       float v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + vcol] + bb;
+      for (int e = 0; e < 8; ++e) v[e] = Cs[(r + e) * LDC + vcl] + bb;
       Vec8<T> o; o.from_float(v);
       o.store(vt + (int64_t)(vh * d_head + vi) * n_pad + gm);
     }
