@@ -12,10 +12,11 @@
 // A workgroup owns 128 queries of one head (32 per wave).  Scores are formed
 // transposed, S^T = K Q^T, with 32x32 MFMA atoms, so that each lane holds the
 // scores of one query: the online-softmax max and sum are register
-// reductions plus one exchange with lane ^ 32.  The K rows of each 32-key
-// sub-tile are fed to the MFMA in an order (bits 2 and 3 of the row index
-// swapped) that makes the score accumulator registers coincide with the B
-// operand of the P V product, so probabilities never leave registers.
+// reductions plus one in-register exchange with lane ^ 32.  The K rows of
+// each 32-key sub-tile are fed to the MFMA in an order (bits 2 and 3 of the
+// row index swapped) that makes the score accumulator registers coincide
+// with the B operand of the P V product, so probabilities never leave
+// registers.
 // V arrives transposed (vt[head][d][token]) from the QKV epilogue, so the
 // A operand of O^T = V^T P^T is a contiguous 16-byte read.  K and V^T tiles
 // stream through a four-stage LDS ring filled by global_load_lds.  The
@@ -283,14 +284,14 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     float ts = 0.f;
     if (!__all(m_ref == -INFINITY)) ts = probs(std::false_type{}, 0.f);
     int exact = m_ref == -INFINITY || !(ts <= kMaxTileSum);
-    exact |= __shfl_xor(exact, 32, WAVE);
+    exact = halves_or(exact);
     if (exact) {
       float mx = -INFINITY;
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[rt][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      mx = halves_max(mx);
       const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
       const float m_new = fmaxf(m_ref, mx + m_use);
       const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_ref - m_new);
@@ -347,7 +348,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mt);
   const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mt);
   const float lpart = lsum * a0 + l1 * a1;
-  const float total = lpart + __shfl_xor(lpart, 32, WAVE);
+  const float total = halves_sum(lpart);
   const float inv = 1.0f / total;
   T* orow = O + (int64_t)q * d_b + head * D;
 #pragma unroll

@@ -167,20 +167,46 @@ struct Swz {
 __device__ __forceinline__ int swz128(int row) { return (row >> 1) & 7; }
 
 // --------------------------------------------------------- reductions
+// Lane l combined with lane l ^ 32 by a commutative operation.
+// v_permlane32_swap exchanges the two 32-lane halves of a pair of registers
+// without an LDS round trip; given x twice it leaves the lower half's value
+// in one result and the upper half's in the other on every lane, so both
+// lanes of a pair compute op(lower, upper) and agree bit for bit.  Both
+// lanes of a pair must be active.
+__device__ __forceinline__ float2 wave_halves(float x) {
+  const auto v = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const float2 h = wave_halves(x);
+  return h.x + h.y;
+}
+__device__ __forceinline__ float halves_max(float x) {
+  const float2 h = wave_halves(x);
+  return fmaxf(h.x, h.y);
+}
+__device__ __forceinline__ int halves_or(int x) {
+  const auto v = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
+  return (int)(v[0] | v[1]);
+}
+// Sum over the wave, the same value on every lane, by register exchanges
+// only: within each 16-lane row, DPP partners at lane ^ 1 and lane ^ 2
+// (quad permutes), then the mirror images within 8 and within 16 lanes
+// (each step pairs groups that already hold equal partial sums); then the
+// rows in pairs (v_permlane16_swap) and the halves (v_permlane32_swap).
+// All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-  return v;
-}
-__device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, WAVE));
-  return v;
-}
-__device__ __forceinline__ int wave_max(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, WAVE));
-  return v;
+  v += dpp_mov<0xB1>(v);    // quad_perm(1, 0, 3, 2): lane ^ 1
+  v += dpp_mov<0x4E>(v);    // quad_perm(2, 3, 0, 1): lane ^ 2
+  v += dpp_mov<0x141>(v);   // row_half_mirror: lane 7 - i within 8
+  v += dpp_mov<0x140>(v);   // row_mirror: lane 15 - i within 16
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  return halves_sum(v);
 }
 
 // GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf(z) taken as
