@@ -476,7 +476,7 @@ struct CallOpts {
 template <typename T>
 cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t n_chunks,
                       const int32_t* req, int32_t n_req, const T* emb, const cr_dims* d,
-                      const char* prep, char* ws, int64_t N, int max_len, const CallOpts& opt,
+                      const char* prep, char* ws, int64_t N, const CallOpts& opt,
                       hipStream_t s) {
   const Prepared P = prepared_layout(d, l);
   const Workspace W = workspace_layout(d, l, N);
@@ -532,7 +532,7 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
       return cr::chunk_schedule(off, n_chunks, req, n_req, opt.mask, opt.pos_offset, lo, hi, pos,
                                 gpos, flags, s); }));
   CR_TRY(timed("rope_table", s, [&] {
-      return cr::rope_table(rope, max_len, dhd, (double)d->rope_theta, s); }));
+      return cr::rope_table(rope, pos, (int)M, dhd, (double)d->rope_theta, s); }));
   if (opt.place_keys)
     CR_TRY(timed("key_rope_table", s, [&] {
         return cr::key_rope_table(krope, gpos, M, opt.kr, s); }));
@@ -567,7 +567,7 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
         return cr::layernorm<T>(h, db, a, db, PF(Bk.ln1_g), PF(Bk.ln1_b), M, db, eps, s); }));
     CR_TRY(timed("gemm_qkv", s, [&] {
         return cr::gemm_qkv<T>(a, db, PT(Bk.w_qkv), M, db, db, dhd, q, k, vt, W.n_pad, PF(Bk.b_qkv),
-                           pos, rope, s); }));
+                           rope, s); }));
     CR_TRY(timed("attention", s, [&] {
         return cr::attention<T>(q, k, vt, o, M, db, nh, dhd, W.n_pad, lo, hi, s); }));
     CR_TRY(timed("gemm_oproj", s, [&] {
@@ -732,7 +732,6 @@ namespace {
 struct Call {
   CallOpts opt;
   int64_t N = 0;
-  int max_len = 0;
 };
 
 bool same_shape(const cr_kv_layout* a, const cr_kv_layout* b) {
@@ -801,15 +800,6 @@ cr_status validate_call(const void* kv, const cr_kv_layout* layout, const int32_
       (!static_ws && !aligned(workspace, ALIGN)))
     return CR_ERR_WORKSPACE;
   c->N = N;
-  int max_len = 0;
-  if (request_chunks) {
-    for (int r = 0; r < n_requests; ++r)
-      max_len = std::max(max_len, chunk_offsets[request_chunks[r + 1]] -
-                                      chunk_offsets[request_chunks[r]]);
-  } else {
-    max_len = (int)N;
-  }
-  c->max_len = max_len;
   return CR_OK;
 }
 
@@ -822,11 +812,11 @@ cr_status enqueue_call(void* kv, const cr_kv_layout* layout, const int32_t* chun
     return repair_impl<bf16>(static_cast<bf16*>(kv), layout, chunk_offsets, n_chunks,
                              request_chunks, n_requests, static_cast<const bf16*>(token_embeds),
                              dims, static_cast<const char*>(prepared),
-                             static_cast<char*>(workspace), c.N, c.max_len, c.opt, s);
+                             static_cast<char*>(workspace), c.N, c.opt, s);
   return repair_impl<float>(static_cast<float*>(kv), layout, chunk_offsets, n_chunks,
                             request_chunks, n_requests, static_cast<const float*>(token_embeds),
                             dims, static_cast<const char*>(prepared),
-                            static_cast<char*>(workspace), c.N, c.max_len, c.opt, s);
+                            static_cast<char*>(workspace), c.N, c.opt, s);
 }
 
 // staging of the pipeline: per slot the cache [L][2][n][H][d_h] and the

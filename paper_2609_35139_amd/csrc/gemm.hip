@@ -153,10 +153,10 @@ template <typename T>
 struct EpiQKV {
   static constexpr bool kWide = false;   // head-aligned 128-column tiles
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
-  T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
-  const float2* rope;
+  T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias;
+  const float2* rope;   // (cos, sin) per token
   template <int ROWS, int COLS, int NT>
-  struct Pre { float bx[8], by[8]; int pp[SegMap<ROWS, COLS, NT>::PASSES]; };
+  struct Pre { float bx[8], by[8]; };
   template <int ROWS, int COLS, int NT>
   __device__ void prefetch(Pre<ROWS, COLS, NT>& p, int m0, int n0, int M, int N) const {
     if (n0 >= 2 * d_b) return;      // V tiles load their bias per column in run()
@@ -166,11 +166,6 @@ struct EpiQKV {
     const int pc = hc < half ? c + half : c - half;
     load8f(bias + n0 + c, p.bx);
     load8f(bias + n0 + pc, p.by);
-#pragma unroll
-    for (int q = 0; q < S::PASSES; ++q) {
-      const int gm = m0 + S::row(q);
-      p.pp[q] = gm < M ? pos[gm] : 0;
-    }
   }
   template <int ROWS, int COLS, int LDC, int NT>
   __device__ void run(const float* Cs, const Pre<ROWS, COLS, NT>& p, int m0, int n0, int M,
@@ -202,8 +197,10 @@ struct EpiQKV {
       float4 cs[GRP][4];
 #pragma unroll
       for (int q = 0; q < GRP; ++q) {
+        // rows past M (K padding) take token 0's rotation: finite, never used
+        const int gm = m0 + S::row(q0 + q);
         const float4* t4 =
-            reinterpret_cast<const float4*>(rope + (int64_t)p.pp[q0 + q] * half + fi);
+            reinterpret_cast<const float4*>(rope + (int64_t)(gm < M ? gm : 0) * half + fi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) cs[q][e] = t4[e];
       }
@@ -258,8 +255,8 @@ struct EpiQKV {
 template <typename T>
 struct EpiQKVh {
   static constexpr bool kWide = true;
-  T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias; const int* pos;
-  const float2* rope;
+  T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias;
+  const float2* rope;   // (cos, sin) per token
   __device__ int b_row(int n) const {
     const int g3 = 3 * d_head, rem = n % g3;
     return (rem / d_head) * d_b + (n / g3) * d_head + rem % d_head;
@@ -299,8 +296,8 @@ struct EpiQKVh {
     g.col_ok = n0 + g.c < N;
     return g;
   }
-  // The pass's positions, (cos, sin) entries and biases are loaded before the
-  // pass's tile is staged, so their latency hides behind the staging.
+  // The pass's (cos, sin) entries and biases are loaded before the pass's
+  // tile is staged, so their latency hides behind the staging.
   template <int ROWS, int COLS, int NT>
   struct Pre {
     float bx[8], by[8], bb;
@@ -319,17 +316,14 @@ struct EpiQKVh {
     using MP = Map<ROWS, COLS, NT>;
     const Seg g = seg<MP::QK_SEGS>(n0, N);
     const int half = d_head / 2;
-    int p[MP::QK_ITEMS];
-#pragma unroll
-    for (int j = 0; j < MP::QK_ITEMS; ++j) {
-      const int gm = m0 + threadIdx.x / MP::QK_SEGS + j * (NT / MP::QK_SEGS);
-      p[j] = gm < M ? pos[gm] : 0;
-    }
     const int bcol = g.part * d_b + g.hh * d_head;
     if (g.col_ok) { load8f(bias + bcol + g.i, pr.bx); load8f(bias + bcol + g.pi, pr.by); }
 #pragma unroll
     for (int j = 0; j < MP::QK_ITEMS; ++j) {
-      const float4* src = reinterpret_cast<const float4*>(rope + (int64_t)p[j] * half + g.fi);
+      // rows past M (K padding) take token 0's rotation: finite, never used
+      const int gm = m0 + threadIdx.x / MP::QK_SEGS + j * (NT / MP::QK_SEGS);
+      const float4* src =
+          reinterpret_cast<const float4*>(rope + (int64_t)(gm < M ? gm : 0) * half + g.fi);
 #pragma unroll
       for (int e = 0; e < 4; ++e) pr.t4[j][e] = src[e];
     }
@@ -790,11 +784,10 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
     epi.template run<ER, G::BN, G::LDC, G::NT>(Cs, pre, m0, n0, M, N);
     return;
   }
-#pragma unroll
-  for (int part = 0; part < G::BM / ER; ++part) {
-    if (part > 0 || !(G::EARLY || G::EARLY2))
-      epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
-    __syncthreads();  // ring (or the previous pass's rows) no longer read
+  // the accumulator rows of staging pass `part`, written over the ring (or
+  // the previous pass's rows) once nobody reads it
+  auto stage = [&](int part) {
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < G::TM; ++i) {
       const int r0 = wm + i * 32 - part * ER;   // first row of atom row i in this pass
@@ -809,6 +802,12 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
                           acc[i][j][4 * g + 3]);
     }
     __syncthreads();
+  };
+#pragma unroll
+  for (int part = 0; part < G::BM / ER; ++part) {
+    if (part > 0 || !(G::EARLY || G::EARLY2))
+      epi.template prefetch<ER, G::BN, G::NT>(pre, m0 + part * ER, n0, M, N);
+    stage(part);
     epi.template run<ER, G::BN, G::LDC, G::NT>(Cs, pre, m0 + part * ER, n0, M, N);
   }
 }
@@ -886,8 +885,8 @@ hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, in
 
 template <typename T>
 hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
-                    T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
-                    const float2* rope, hipStream_t s) {
+                    T* q, T* k, T* vt, int64_t n_pad, const float* bias, const float2* rope,
+                    hipStream_t s) {
   const int N = 3 * d_b;
   // 192-column tiles of whole heads on a 256x192 grid (eight waves of 64x96)
   // when it fills its rounds well enough; otherwise 128x128 tiles in the
@@ -899,11 +898,11 @@ hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, 
     const int64_t tiles128 = (int64_t)((M + 127) / 128) * (N / 128);
     const double fill128 = tiles128 <= 256 ? round_fill(tiles128, 256) : round_fill(tiles128, 512);
     if (192 % (3 * d_head) == 0 && N % 192 == 0 && kWideGain * round_fill(wide, 256) >= fill128) {
-      EpiQKVh<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
+      EpiQKVh<T> e{q, k, vt, n_pad, d_b, d_head, bias, rope};
       return launch_tiled<T, GemmTile<T, 2, 3, 2, 4, 2>>(A, lda, B, K, M, N, K, e, s);
     }
   }
-  EpiQKV<T> e{q, k, vt, n_pad, d_b, d_head, bias, pos, rope};
+  EpiQKV<T> e{q, k, vt, n_pad, d_b, d_head, bias, rope};
   return launch<T>(A, lda, B, K, M, N, K, e, s);
 }
 
@@ -947,7 +946,7 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
                                    int64_t, const float*, const T*, int64_t, bool, hipStream_t, \
                                    const T*, int64_t);                                          \
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*, \
-                                  int64_t, const float*, const int*, const float2*, hipStream_t); \
+                                  int64_t, const float*, const float2*, hipStream_t);            \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides, \
                                      const float*, const float*, int, const int*,               \
                                      const float2*, T*, KvStrides, hipStream_t);

@@ -59,8 +59,8 @@ hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, in
 // (finite padding); V is written transposed, vt[head][d][n_pad].
 template <typename T>
 hipError_t gemm_qkv(const T* A, int64_t lda, const T* B, int M, int K, int d_b, int d_head,
-                    T* q, T* k, T* vt, int64_t n_pad, const float* bias, const int* pos,
-                    const float2* rope, hipStream_t s);
+                    T* q, T* k, T* vt, int64_t n_pad, const float* bias, const float2* rope,
+                    hipStream_t s);
 
 // KV residual head fused with the output add into the strided cache, for
 // coordinates j in [0, D_KV) of the selected components:
@@ -124,8 +124,9 @@ template <typename T>
 hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* tab, bool inverse,
                        float scale, hipStream_t s);
 
-// ---- RoPE (cos, sin) table for positions [0, max_pos), computed in fp64.
-hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStream_t s);
+// ---- RoPE (cos, sin) table per token: tab[t][i] = (cos, sin)(pos[t] * f_i),
+// f_i = theta^(-2i / d_head), i < d_head / 2, computed in fp64.
+hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s);
 
 // ---- weight preparation
 // dst[b][c][r] = src[b][r][c] / div[b][r] for r < R, c < C; zero for

@@ -409,21 +409,24 @@ template hipError_t rotate_keys<float>(float*, KvStrides, int, int, const float2
                                        hipStream_t);
 
 // ------------------------------------------------------------ RoPE table
-__global__ __launch_bounds__(256) void rope_table_kernel(float2* tab, int max_pos, int half,
-                                                         int d_head, double theta) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= max_pos * half) return;
-  const int p = idx / half, i = idx % half;
-  const double ang = (double)p * pow(theta, -2.0 * (double)i / (double)d_head);
+// One row per token, so that the QKV epilogue's table reads do not wait for
+// a position load first.
+__global__ __launch_bounds__(256) void rope_table_kernel(float2* __restrict__ tab,
+                                                         const int* __restrict__ pos, int N,
+                                                         int half, int d_head, double theta) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)N * half) return;
+  const int t = (int)(idx / half), i = (int)(idx % half);
+  const double ang = (double)pos[t] * pow(theta, -2.0 * (double)i / (double)d_head);
   tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
 }
 
-hipError_t rope_table(float2* tab, int max_pos, int d_head, double theta, hipStream_t s) {
+hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s) {
   const int half = d_head / 2;
-  const int n = max_pos * half;
+  const int64_t n = (int64_t)N * half;
   if (n <= 0) return hipSuccess;
-  CR_LAUNCH(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos,
-                     half, d_head, theta);
+  CR_LAUNCH(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tab, pos, N,
+            half, d_head, theta);
   return hipGetLastError();
 }
 

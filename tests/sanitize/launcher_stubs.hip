@@ -13,7 +13,9 @@ hipError_t chunk_schedule(const int32_t*, int32_t, const int32_t*, int32_t, int,
 hipError_t key_rope_table(float2*, const int*, int, const KeyRope&, hipStream_t) {
   return hipErrorInvalidValue;
 }
-hipError_t rope_table(float2*, int, int, double, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t rope_table(float2*, const int*, int, int, double, hipStream_t) {
+  return hipErrorInvalidValue;
+}
 
 template <typename T>
 hipError_t gemm_bias(const T*, int64_t, const T*, int64_t, int, int, int, T*, int64_t,
@@ -22,7 +24,7 @@ hipError_t gemm_bias(const T*, int64_t, const T*, int64_t, int, int, int, T*, in
 }
 template <typename T>
 hipError_t gemm_qkv(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*, int64_t,
-                    const float*, const int*, const float2*, hipStream_t) {
+                    const float*, const float2*, hipStream_t) {
   return hipErrorInvalidValue;
 }
 template <typename T>
@@ -64,7 +66,7 @@ hipError_t convert_f32(const Tin*, float*, int64_t, int64_t, int, int64_t, int64
                                    int64_t, const float*, const T*, int64_t, bool, hipStream_t,   \
                                    const T*, int64_t);                                            \
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*,   \
-                                  int64_t, const float*, const int*, const float2*, hipStream_t); \
+                                  int64_t, const float*, const float2*, hipStream_t);             \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides,   \
                                      const float*, const float*, int, const int*, const float2*,  \
                                      T*, KvStrides, hipStream_t);                                 \
