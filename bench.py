@@ -23,7 +23,7 @@ PEAK = {"bf16_tflops": 2500.0, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
 
 # kernel class (as reported by cr_profile_read) -> kernel function it launches
 FUNCTION_OF = {
-    "gemm_compress": "gemm_nt_kernel<EpiBias>", "gemm_token": "gemm_nt_kernel<EpiBias>",
+    "gemm_compress": "gemm_nt_kernel<EpiBias>",
     "gemm_fuse": "gemm_nt_kernel<EpiBias>", "gemm_inject": "gemm_nt_kernel<EpiBias>",
     "gemm_oproj": "gemm_nt_kernel<EpiBias>", "gemm_ffn1": "gemm_nt_kernel<EpiBias>",
     # the QKV projection runs on 256x192 tiles of whole heads (EpiQKVh) or on
@@ -50,7 +50,9 @@ def allowed_pairs(w):
 def algorithmic_work(w):
     """Per-step algorithmic FLOPs and HBM bytes of every kernel class.
 
-    Weights are counted once per launch; attention counts only allowed
+    Weights are counted once per launch; the fusion counts the composed map
+    [s ; e] -> h^0 that the library applies (the token projection's weights
+    are folded into it when the weights are prepared); attention counts only allowed
     pairs (QK^T and PV, 2 FLOPs per MAC).  The two cache-streaming steps
     count only what the method must move: the stage-1 compression reads the
     stale cache once (its per-segment outputs are an intermediate, not
@@ -66,8 +68,8 @@ def algorithmic_work(w):
     work = {
         "compress_segments": (2.0 * N * D * r.d_seg, es * N * D, 1),
         "gemm_compress": (*gemm(dc, kc), 1),
-        "gemm_token": (*gemm(db, E), 1),
-        "gemm_fuse": (*gemm(db, dc + db), 1),
+        # token projection composed into the fusion: one product of [s ; e]
+        "gemm_fuse": (*gemm(db, dc + E), 1),
         "gemm_inject": (*gemm(B * db, dc), 1),         # all blocks' P_b(s) in one launch
         "gemm_qkv": tuple(x * B for x in gemm(3 * db, db)) + (B,),
         "attention": (4.0 * allowed_pairs(w) * db * B, es * 4 * N * db * B, B),

@@ -42,7 +42,11 @@
  *  - Weights reach the repair calls as the prepared buffer that
  *    cr_prepare_weights builds once from the canonical blob (matrices
  *    transposed to [out][in], 1/sigma_stale folded in, vectors widened to
- *    fp32), so no call converts weights; the canonical blob described by
+ *    fp32, and the token projection composed into the fusion: both are
+ *    affine with nothing between them, so [s ; t] W_fuse with
+ *    t = e W_tok + b_tok is applied as one product of [s ; e], its weights
+ *    W_tok W_fuse_t formed on the device and rounded once to the storage
+ *    dtype), so no call converts weights; the canonical blob described by
  *    cr_weights_layout stays the one interchange format.
  *  - No exceptions cross the ABI.  Entry points are reentrant given distinct
  *    workspaces.

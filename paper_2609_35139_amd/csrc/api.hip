@@ -258,11 +258,13 @@ struct BlockP {
 // layout, so block b's offsets are block 0's plus b times the block stride.
 struct Prepared {
   int64_t kc, kc_pad;
-  uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_tok, b_tok, w_fuse, b_fuse;
+  uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_fuse, b_fuse;
   uint64_t w_inj, b_inj;
   BlockP blk0;
   uint64_t blk_stride;
-  uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta, total;
+  uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta;
+  uint64_t tmp;   // scratch of the preparation itself
+  uint64_t total;
   BlockP blk(int b) const {
     const uint64_t o = (uint64_t)b * blk_stride;
     const BlockP& q = blk0;
@@ -283,8 +285,9 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
   p.b_seg = a.take(S * 32 * F);
   p.w_cmp = a.take(dc * p.kc_pad * T);
   p.b_cmp = a.take(dc * F); p.ln_enc_g = a.take(dc * F); p.ln_enc_b = a.take(dc * F);
-  p.w_tok = a.take(db * E * T); p.b_tok = a.take(db * F);
-  p.w_fuse = a.take(db * (dc + db) * T); p.b_fuse = a.take(db * F);
+  // the fusion [s ; t] W_fuse with t = e W_tok + b_tok, composed into one
+  // map of [s ; e]: [W_fuse_s ; W_tok W_fuse_t], bias b_fuse + b_tok W_fuse_t
+  p.w_fuse = a.take(db * (dc + E) * T); p.b_fuse = a.take(db * F);
   p.w_inj = a.take(d->n_blocks * db * dc * T); p.b_inj = a.take(d->n_blocks * db * F);
   const uint64_t first = a.off;
   for (int b = 0; b < d->n_blocks; ++b) {
@@ -303,6 +306,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
   if (d->n_blocks == 0) p.blk_stride = 0;
   p.ln_f_g = a.take(db * F); p.ln_f_b = a.take(db * F);
   p.w_out = a.take(D * db * T); p.b_out = a.take(D * F); p.sigma_delta = a.take(D * F);
+  p.tmp = a.take(db * db * T + E * F);
   p.total = a.off;
   return p;
 }
@@ -321,7 +325,7 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   Workspace w;
   w.n = N;
   w.n_pad = round_up(std::max<int64_t>(N, 1), 128);
-  w.ldst = dc + db;
+  w.ldst = dc;
   w.ldinj = (int64_t)d->n_blocks * db;
   Arena a;
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
@@ -427,10 +431,22 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
   CR_TRY(vec("b_cmp", p.b_cmp, dc));
   CR_TRY(vec("ln_enc_g", p.ln_enc_g, dc));
   CR_TRY(vec("ln_enc_b", p.ln_enc_b, dc));
-  CR_TRY(mat("w_tok", p.w_tok, E, db, E));
-  CR_TRY(vec("b_tok", p.b_tok, db));
-  CR_TRY(mat("w_fuse", p.w_fuse, dc + db, db, dc + db));
-  CR_TRY(vec("b_fuse", p.b_fuse, db));
+  // token projection composed into the fusion (both affine, nothing between
+  // them): the s columns of W_fuse^T first (the e columns zero-filled), then
+  // (W_tok W_fuse_t)^T = W_fuse_t^T W_tok^T into the e columns, formed by the
+  // library GEMM from W_fuse_t^T (in tmp) and W_tok (canonical [E][d_b]),
+  // rounded once to the storage type; the bias is composed in fp32
+  T* wf = reinterpret_cast<T*>(out + p.w_fuse);
+  T* wft = reinterpret_cast<T*>(out + p.tmp);
+  float* zero = reinterpret_cast<float*>(out + p.tmp + (uint64_t)db * db * sizeof(T));
+  CR_TRY(cr::transpose_convert<T, T>(src("w_fuse"), wf, 1, dc, db, db, dc + E, nullptr, s));
+  CR_TRY(cr::transpose_convert<T, T>(src("w_fuse") + (int64_t)dc * db, wft, 1, db, db, db, db,
+                                     nullptr, s));
+  CR_TRY(cr::convert_f32<T>(src("b_tok"), zero, 0, E, 1, 0, 0, s));
+  CR_TRY(cr::gemm_bias<T>(wft, db, src("w_tok"), db, db, E, db, wf + dc, dc + E, zero, nullptr, 0,
+                          false, s));
+  CR_TRY(cr::compose_bias<T>(src("b_tok"), src("w_fuse") + (int64_t)dc * db, db, src("b_fuse"),
+                             reinterpret_cast<float*>(out + p.b_fuse), db, db, s));
   for (int b = 0; b < d->n_blocks; ++b) {
     const std::string q = "blk" + std::to_string(b) + ".";
     const BlockP B = p.blk(b);
@@ -552,13 +568,11 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
     CR_TRY(timed("gemm_inject", s, [&] {
         return cr::gemm_bias<T>(st, ldst, PT(P.w_inj), dc, M, B * db, dc, inj, ldinj,
                                 PF(P.b_inj), nullptr, 0, false, s); }));
-  // token projection -> st[:, d_c:]; fusion -> h^0, plus block 0's reinjection
-  CR_TRY(timed("gemm_token", s, [&] {
-      return cr::gemm_bias<T>(emb, E, PT(P.w_tok), E, M, db, E, st + dc, ldst, PF(P.b_tok), nullptr,
-                          0, false, s); }));
+  // token projection and fusion as one product of [s ; e] -> h^0, plus
+  // block 0's reinjection
   CR_TRY(timed("gemm_fuse", s, [&] {
-      return cr::gemm_bias<T>(st, ldst, PT(P.w_fuse), dc + db, M, db, dc + db, h, db, PF(P.b_fuse),
-                          rj ? inj : nullptr, ldinj, false, s); }));
+      return cr::gemm_bias_split<T>(st, ldst, dc, emb, E, PT(P.w_fuse), dc + E, M, db, dc + E, h, db,
+                                    PF(P.b_fuse), rj ? inj : nullptr, ldinj, s); }));
   // h holds x_b = h^{b-1} + P_b(s) on entry to block b, h^B after the last block
   for (int b = 0; b < B; ++b) {
     const BlockP Bk = P.blk(b);

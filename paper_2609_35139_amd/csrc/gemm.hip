@@ -635,10 +635,21 @@ __device__ __forceinline__ void tile_of(int M, int N, int& tm, int& tn) {
   tn = k / rows;
 }
 
-template <typename T, typename G, typename Epi>
+// A split along K into two row-major matrices: columns [0, k1) of the
+// product's A come from A (lda), columns [k1, K) from a2 (lda2), so that
+// C = [A | a2] B^T needs no concatenated copy.  k1 is a multiple of the slab.
+template <typename T>
+struct ASplit {
+  const T* a2 = nullptr;
+  int64_t lda2 = 0;
+  int k1 = 0;
+};
+
+template <typename T, typename G, typename Epi, bool SPLIT = false>
 __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A, int64_t lda,
                                                       const T* __restrict__ B, int64_t ldb,
-                                                      int M, int N, int K, Epi epi) {
+                                                      int M, int N, int K, Epi epi,
+                                                      ASplit<T> sp) {
   using MM = Mma32<T>;
   using frag = typename MM::frag;
   __shared__ __align__(1024) char smem[G::LDS];
@@ -662,6 +673,18 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
     const int chunk = (lane & 7) ^ swz128(row);
     asrc[r] = reinterpret_cast<const char*>(A + (int64_t)min(m0 + row, M - 1) * lda) + chunk * 16;
   }
+  // the same rows of the second A matrix, read from slab k1 / BK on
+  const char* asrc2[SPLIT ? G::A_ROUNDS : 1];
+  const int kt1 = SPLIT ? sp.k1 / G::BK : 0;
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int r = 0; r < G::A_ROUNDS; ++r) {
+      const int row = (r * G::NW + wave) * 8 + (lane >> 3);
+      const int chunk = (lane & 7) ^ swz128(row);
+      asrc2[r] = reinterpret_cast<const char*>(sp.a2 + (int64_t)min(m0 + row, M - 1) * sp.lda2) +
+                 chunk * 16;
+    }
+  }
 #pragma unroll
   for (int r = 0; r < G::B_ROUNDS; ++r) {
     const int row = (r * G::NW + wave) * 8 + (lane >> 3);
@@ -672,7 +695,13 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   auto issue = [&](int kt, int stage) {
     char* base = smem + stage * G::STAGE_BYTES;
 #pragma unroll
-    for (int r = 0; r < G::A_ROUNDS; ++r) dma16(asrc[r] + kt * 128, base + (r * G::NW + wave) * 1024);
+    for (int r = 0; r < G::A_ROUNDS; ++r) {
+      const char* a = asrc[r] + kt * 128;
+      if constexpr (SPLIT) {
+        if (kt >= kt1) a = asrc2[r] + (kt - kt1) * 128;
+      }
+      dma16(a, base + (r * G::NW + wave) * 1024);
+    }
 #pragma unroll
     for (int r = 0; r < G::B_ROUNDS; ++r)
       dma16(bsrc[r] + kt * 128, base + G::BM * 128 + (r * G::NW + wave) * 1024);
@@ -812,19 +841,22 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
   }
 }
 
-template <typename T, typename G, typename Epi>
+template <typename T, typename G, typename Epi, bool SPLIT = false>
 static hipError_t launch_tiled(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N,
-                               int K, const Epi& epi, hipStream_t s) {
+                               int K, const Epi& epi, hipStream_t s, ASplit<T> sp = {}) {
   if (M <= 0 || N <= 0) return hipSuccess;
   // the main loop streams whole 128-byte K slabs with 16-byte copies
   if (K <= 0 || K % G::BK != 0 || lda % G::VEC != 0 || ldb % G::VEC != 0 ||
       reinterpret_cast<uintptr_t>(A) % 16 != 0 || reinterpret_cast<uintptr_t>(B) % 16 != 0)
     return hipErrorInvalidValue;
+  if (SPLIT && (!sp.a2 || sp.k1 <= 0 || sp.k1 >= K || sp.k1 % G::BK != 0 ||
+                sp.lda2 % G::VEC != 0 || reinterpret_cast<uintptr_t>(sp.a2) % 16 != 0))
+    return hipErrorInvalidValue;
   const int64_t tiles = (int64_t)((N + G::BN - 1) / G::BN) * ((M + G::BM - 1) / G::BM);
   if (tiles >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
   dim3 grid((unsigned)tiles);
-  CR_LAUNCH((gemm_nt_kernel<T, G, Epi>), grid, dim3(G::NT), 0, s, A, lda, B, ldb, M, N, K,
-                     epi);
+  CR_LAUNCH((gemm_nt_kernel<T, G, Epi, SPLIT>), grid, dim3(G::NT), 0, s, A, lda, B, ldb, M, N, K,
+            epi, sp);
   return hipGetLastError();
 }
 
@@ -850,15 +882,16 @@ static inline double round_fill(int64_t tiles, int64_t slots) {
 // outweighs a worse fill of the last round.
 constexpr double kWideGain = 1.25;
 
-template <typename T, typename Epi>
+template <typename T, typename Epi, bool SPLIT = false>
 static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M, int N, int K,
-                         const Epi& epi, hipStream_t s) {
+                         const Epi& epi, hipStream_t s, ASplit<T> sp = {}) {
   if constexpr (sizeof(T) == 2 && Epi::kWide) {
     const int64_t wide_tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
     const int64_t tiles128 = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
     const double fill128 = tiles128 <= 256 ? round_fill(tiles128, 256) : round_fill(tiles128, 512);
     if (kWideGain * round_fill(wide_tiles, 256) >= fill128)
-      return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
+      return launch_tiled<T, GemmTile<T, 4, 2, 2, 2, 4>, Epi, SPLIT>(A, lda, B, ldb, M, N, K, epi, s,
+                                                                    sp);
   }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
   if (tiles <= 256) {
@@ -868,11 +901,13 @@ static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M
     // partial-tile sum costs more than it saves)
     if constexpr (sizeof(T) == 2) {
       if (K >= 2048)
-        return launch_tiled<T, GemmTile<T, 2, 2, 4, 2, 2, false, 2>>(A, lda, B, ldb, M, N, K, epi, s);
+        return launch_tiled<T, GemmTile<T, 2, 2, 4, 2, 2, false, 2>, Epi, SPLIT>(A, lda, B, ldb, M, N,
+                                                                                K, epi, s, sp);
     }
-    return launch_tiled<T, GemmTile<T, 2, 1, 4, 2, 4>>(A, lda, B, ldb, M, N, K, epi, s);
+    return launch_tiled<T, GemmTile<T, 2, 1, 4, 2, 4>, Epi, SPLIT>(A, lda, B, ldb, M, N, K, epi, s,
+                                                                 sp);
   }
-  return launch_tiled<T, GemmTile<T, 2, 2, 2>>(A, lda, B, ldb, M, N, K, epi, s);
+  return launch_tiled<T, GemmTile<T, 2, 2, 2>, Epi, SPLIT>(A, lda, B, ldb, M, N, K, epi, s, sp);
 }
 
 template <typename T>
@@ -881,6 +916,14 @@ hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, in
                      bool gelu, hipStream_t s, const T* resid2, int64_t ldr2) {
   EpiBias<T> e{out, ldo, bias, resid, ldr, resid2, ldr2, gelu ? 1 : 0};
   return launch<T>(A, lda, B, ldb, M, N, K, e, s);
+}
+
+template <typename T>
+hipError_t gemm_bias_split(const T* A, int64_t lda, int K1, const T* A2, int64_t lda2, const T* B,
+                           int64_t ldb, int M, int N, int K, T* out, int64_t ldo,
+                           const float* bias, const T* resid, int64_t ldr, hipStream_t s) {
+  EpiBias<T> e{out, ldo, bias, resid, ldr, nullptr, 0, 0};
+  return launch<T, EpiBias<T>, true>(A, lda, B, ldb, M, N, K, e, s, ASplit<T>{A2, lda2, K1});
 }
 
 template <typename T>
@@ -945,6 +988,9 @@ hipError_t gemm_expand(const T* A, int64_t lda, const T* B, int M, int N, int K,
   template hipError_t gemm_bias<T>(const T*, int64_t, const T*, int64_t, int, int, int, T*,    \
                                    int64_t, const float*, const T*, int64_t, bool, hipStream_t, \
                                    const T*, int64_t);                                          \
+  template hipError_t gemm_bias_split<T>(const T*, int64_t, int, const T*, int64_t, const T*,   \
+                                         int64_t, int, int, int, T*, int64_t, const float*,      \
+                                         const T*, int64_t, hipStream_t);                        \
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*, \
                                   int64_t, const float*, const float2*, hipStream_t);            \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides, \

@@ -53,8 +53,15 @@ hipError_t gemm_bias(const T* A, int64_t lda, const T* B, int64_t ldb, int M, in
                      T* out, int64_t ldo, const float* bias, const T* resid, int64_t ldr,
                      bool gelu, hipStream_t s, const T* resid2 = nullptr, int64_t ldr2 = 0);
 
+// The same with A split along K: C = [A | A2] B^T + bias (+ resid), A
+// supplying columns [0, K1) and A2 columns [K1, K); K1 % 64 == 0.
+template <typename T>
+hipError_t gemm_bias_split(const T* A, int64_t lda, int K1, const T* A2, int64_t lda2, const T* B,
+                           int64_t ldb, int M, int N, int K, T* out, int64_t ldo,
+                           const float* bias, const T* resid, int64_t ldr, hipStream_t s);
+
 // QKV projection with the repair backbone's RoPE on Q and K (rotate-half
-// pairs, table rope[pos][d_head/2] of (cos, sin)); Q is written scaled by
+// pairs, table rope[token][d_head/2] of (cos, sin)); Q is written scaled by
 // log2(e)/sqrt(d_head); K rows and V^T columns are written up to n_pad
 // (finite padding); V is written transposed, vt[head][d][n_pad].
 template <typename T>
@@ -129,6 +136,10 @@ hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* t
 hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s);
 
 // ---- weight preparation
+// out[n] = add[n] + sum_k v[k] * W[k][n] (W row-major [K][ldw]), in fp32.
+template <typename T>
+hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, float* out, int K,
+                        int N, hipStream_t s);
 // dst[b][c][r] = src[b][r][c] / div[b][r] for r < R, c < C; zero for
 // r in [R, ld_dst) and c in [C, Cp).
 template <typename Tin, typename Tout>

@@ -431,6 +431,28 @@ hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double the
 }
 
 // ------------------------------------------------------- weight preparation
+// Bias of two composed affine maps: out[n] = add[n] + sum_k v[k] W[k][n].
+template <typename T>
+__global__ __launch_bounds__(256) void compose_bias_kernel(const T* __restrict__ v,
+                                                           const T* __restrict__ W, int64_t ldw,
+                                                           const T* __restrict__ add,
+                                                           float* __restrict__ out, int K, int N) {
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= N) return;
+  float acc = to_f32(add[n]);
+  for (int k = 0; k < K; ++k) acc = fmaf(to_f32(v[k]), to_f32(W[(int64_t)k * ldw + n]), acc);
+  out[n] = acc;
+}
+
+template <typename T>
+hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, float* out, int K,
+                        int N, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  CR_LAUNCH((compose_bias_kernel<T>), dim3((N + 255) / 256), dim3(256), 0, s, v, W, ldw, add, out,
+            K, N);
+  return hipGetLastError();
+}
+
 template <typename Tin, typename Tout>
 __global__ __launch_bounds__(256) void transpose_convert_kernel(const Tin* __restrict__ src,
                                                                 Tout* __restrict__ dst, int R,
@@ -487,7 +509,9 @@ hipError_t convert_f32(const Tin* src, float* dst, int64_t n, int64_t n_pad, int
   template hipError_t transpose_convert<T, T>(const T*, T*, int, int, int, int, int64_t,        \
                                               const float*, hipStream_t);                       \
   template hipError_t convert_f32<T>(const T*, float*, int64_t, int64_t, int, int64_t, int64_t, \
-                                     hipStream_t);
+                                     hipStream_t);                                              \
+  template hipError_t compose_bias<T>(const T*, const T*, int64_t, const T*, float*, int, int,  \
+                                      hipStream_t);
 CR_INST(bf16)
 CR_INST(float)
 #undef CR_INST

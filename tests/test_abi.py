@@ -181,7 +181,7 @@ def test_schedule_and_prepare_validation():
 def test_workspace_views():
     off_s, ld_s = B.cr_workspace_view(_dims(W0), _layout(W0), 64, "s")
     off_h, ld_h = B.cr_workspace_view(_dims(W0), _layout(W0), 64, "h")
-    assert ld_s == W0.rep.d_c + W0.rep.d_b and ld_h == W0.rep.d_b
+    assert ld_s == W0.rep.d_c and ld_h == W0.rep.d_b
     assert off_s % 256 == 0 and off_h % 256 == 0 and off_s != off_h
     with pytest.raises(B.CrError):
         B.cr_workspace_view(_dims(W0), _layout(W0), 64, "nope")
