@@ -24,7 +24,7 @@ PEAK = {"bf16_tflops": 2500.0, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
 # kernel class (as reported by cr_profile_read) -> kernel function it launches
 FUNCTION_OF = {
     "gemm_compress": "gemm_nt_kernel<EpiBias>",
-    "gemm_fuse": "gemm_nt_kernel<EpiBias>", "gemm_inject": "gemm_nt_kernel<EpiBias>",
+    "gemm_fuse": "gemm_nt_kernel<EpiBias>",
     "gemm_oproj": "gemm_nt_kernel<EpiBias>", "gemm_ffn1": "gemm_nt_kernel<EpiBias>",
     # the QKV projection runs on 256x192 tiles of whole heads (EpiQKVh) or on
     # 128x128 tiles in the weights' column order (EpiQKV), whichever fills
@@ -52,7 +52,9 @@ def algorithmic_work(w):
 
     Weights are counted once per launch; the fusion counts the composed map
     [s ; e] -> h^0 that the library applies (the token projection's weights
-    are folded into it when the weights are prepared); attention counts only allowed
+    are folded into it when the weights are prepared), and each reinjection
+    P_b(s) is counted in the product that applies it (the fusion for block
+    0, block b-1's FFN2 otherwise); attention counts only allowed
     pairs (QK^T and PV, 2 FLOPs per MAC).  The two cache-streaming steps
     count only what the method must move: the stage-1 compression reads the
     stale cache once (its per-segment outputs are an intermediate, not
@@ -70,12 +72,13 @@ def algorithmic_work(w):
         "gemm_compress": (*gemm(dc, kc), 1),
         # token projection composed into the fusion: one product of [s ; e]
         "gemm_fuse": (*gemm(db, dc + E), 1),
-        "gemm_inject": (*gemm(B * db, dc), 1),         # all blocks' P_b(s) in one launch
         "gemm_qkv": tuple(x * B for x in gemm(3 * db, db)) + (B,),
         "attention": (4.0 * allowed_pairs(w) * db * B, es * 4 * N * db * B, B),
         "gemm_oproj": tuple(x * B for x in gemm(db, db)) + (B,),
         "gemm_ffn1": tuple(x * B for x in gemm(m * db, db)) + (B,),
-        "gemm_ffn2": tuple(x * B for x in gemm(db, m * db)) + (B,),
+        # block b's FFN2 also applies P_{b+1}(s): K = m*db + dc but after the last block
+        "gemm_ffn2": (sum(gemm(db, m * db + (dc if b + 1 < B else 0))[0] for b in range(B)),
+                      sum(gemm(db, m * db + (dc if b + 1 < B else 0))[1] for b in range(B)), B),
         "layernorm": (0.0, es * 2 * N * (dc + db * (2 * B + 1)), 2 + 2 * B),
         "gemm_expand": (2.0 * N * db * D, es * (2 * N * D + D * db), 1),
     }

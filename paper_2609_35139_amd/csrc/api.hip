@@ -249,17 +249,22 @@ std::vector<Tensor> canonical(const cr_dims* d, const cr_kv_layout* l, uint64_t*
 }
 
 struct BlockP {
-  uint64_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_ff1, b_ff1, w_ff2, b_ff2;
+  uint64_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_ff1, b_ff1, w_ff2, b_ff2,
+      b_ff2_rj;
 };
 // Prepared (device-optimised) weights: matrices [out][in] in the storage
-// dtype, vectors fp32.  The reinjection projections of all blocks are stacked
-// into one [B*d_b][d_c] matrix so that P_b(s) is computed for every block by
-// a single GEMM.  The blocks' tensors follow one another with the same
-// layout, so block b's offsets are block 0's plus b times the block stride.
+// dtype, vectors fp32.  Each reinjection x_b = h^b + s W_inj_b + b_inj_b
+// follows an affine step with nothing in between, so it is folded into that
+// step's product: block 0's into the fusion (W_fuse_s + W_inj_0 on the s
+// columns), block b's into block b-1's FFN2, whose rows carry d_c more
+// columns (W_inj_b, applied to s: K grows from r*d_b to r*d_b + d_c).  The
+// entrance-only variant uses the plain fusion matrix and the first r*d_b
+// columns of the FFN2 rows.  The blocks' tensors follow one another with the
+// same layout, so block b's offsets are block 0's plus b times the block
+// stride.
 struct Prepared {
   int64_t kc, kc_pad;
-  uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_fuse, b_fuse;
-  uint64_t w_inj, b_inj;
+  uint64_t w_seg, b_seg, w_cmp, b_cmp, ln_enc_g, ln_enc_b, w_fuse, b_fuse, w_fuse_rj, b_fuse_rj;
   BlockP blk0;
   uint64_t blk_stride;
   uint64_t ln_f_g, ln_f_b, w_out, b_out, sigma_delta;
@@ -269,7 +274,8 @@ struct Prepared {
     const uint64_t o = (uint64_t)b * blk_stride;
     const BlockP& q = blk0;
     return BlockP{q.ln1_g + o, q.ln1_b + o, q.w_qkv + o, q.b_qkv + o, q.w_o + o, q.b_o + o,
-                  q.ln2_g + o, q.ln2_b + o, q.w_ff1 + o, q.b_ff1 + o, q.w_ff2 + o, q.b_ff2 + o};
+                  q.ln2_g + o, q.ln2_b + o, q.w_ff1 + o, q.b_ff1 + o, q.w_ff2 + o, q.b_ff2 + o,
+                  q.b_ff2_rj + o};
   }
 };
 
@@ -288,7 +294,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
   // the fusion [s ; t] W_fuse with t = e W_tok + b_tok, composed into one
   // map of [s ; e]: [W_fuse_s ; W_tok W_fuse_t], bias b_fuse + b_tok W_fuse_t
   p.w_fuse = a.take(db * (dc + E) * T); p.b_fuse = a.take(db * F);
-  p.w_inj = a.take(d->n_blocks * db * dc * T); p.b_inj = a.take(d->n_blocks * db * F);
+  p.w_fuse_rj = a.take(db * (dc + E) * T); p.b_fuse_rj = a.take(db * F);   // + block 0's P_0
   const uint64_t first = a.off;
   for (int b = 0; b < d->n_blocks; ++b) {
     BlockP q;
@@ -297,7 +303,7 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
     q.w_o = a.take(db * db * T); q.b_o = a.take(db * F);
     q.ln2_g = a.take(db * F); q.ln2_b = a.take(db * F);
     q.w_ff1 = a.take(r * db * db * T); q.b_ff1 = a.take(r * db * F);
-    q.w_ff2 = a.take(db * r * db * T); q.b_ff2 = a.take(db * F);
+    q.w_ff2 = a.take(db * (r * db + dc) * T); q.b_ff2 = a.take(db * F); q.b_ff2_rj = a.take(db * F);
     if (b == 0) {
       p.blk0 = q;
       p.blk_stride = a.off - first;
@@ -312,8 +318,8 @@ Prepared prepared_layout(const cr_dims* d, const cr_kv_layout* l) {
 }
 
 struct Workspace {
-  int64_t n, n_pad, ldst, ldinj;
-  uint64_t lo, hi, pos, gpos, flags, blocks, blocks_out, rope, krope, U, st, inj, h, a, q, k, vt, o,
+  int64_t n, n_pad, ldst;
+  uint64_t lo, hi, pos, gpos, flags, blocks, blocks_out, rope, krope, U, st, h, a, q, k, vt, o,
       f, total;
 };
 
@@ -326,7 +332,6 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.n = N;
   w.n_pad = round_up(std::max<int64_t>(N, 1), 128);
   w.ldst = dc;
-  w.ldinj = (int64_t)d->n_blocks * db;
   Arena a;
   w.lo = a.take(N * 4); w.hi = a.take(N * 4); w.pos = a.take(N * 4);
   w.gpos = a.take(N * 4); w.flags = a.take(N * 4);
@@ -336,7 +341,6 @@ Workspace workspace_layout(const cr_dims* d, const cr_kv_layout* l, int64_t N) {
   w.krope = a.take(N * (l->head_dim / 2) * 8);        // global key placement table
   w.U = a.take(N * kc_pad * T);
   w.st = a.take(N * w.ldst * T);
-  w.inj = a.take(N * w.ldinj * T);
   w.h = a.take(N * db * T);
   w.a = a.take(N * db * T);
   w.q = a.take(N * db * T);
@@ -436,22 +440,29 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
   // (W_tok W_fuse_t)^T = W_fuse_t^T W_tok^T into the e columns, formed by the
   // library GEMM from W_fuse_t^T (in tmp) and W_tok (canonical [E][d_b]),
   // rounded once to the storage type; the bias is composed in fp32
-  T* wf = reinterpret_cast<T*>(out + p.w_fuse);
+  // (the reinjecting copy's s columns take W_fuse_s + W_inj_0, summed in
+  // fp32 and rounded once, and its bias b_inj_0 too)
   T* wft = reinterpret_cast<T*>(out + p.tmp);
   float* zero = reinterpret_cast<float*>(out + p.tmp + (uint64_t)db * db * sizeof(T));
-  CR_TRY(cr::transpose_convert<T, T>(src("w_fuse"), wf, 1, dc, db, db, dc + E, nullptr, s));
-  CR_TRY(cr::transpose_convert<T, T>(src("w_fuse") + (int64_t)dc * db, wft, 1, db, db, db, db,
-                                     nullptr, s));
+  const T* wfuse_t = src("w_fuse") + (int64_t)dc * db;
+  CR_TRY(cr::transpose_convert<T, T>(wfuse_t, wft, 1, db, db, db, db, nullptr, s));
   CR_TRY(cr::convert_f32<T>(src("b_tok"), zero, 0, E, 1, 0, 0, s));
-  CR_TRY(cr::gemm_bias<T>(wft, db, src("w_tok"), db, db, E, db, wf + dc, dc + E, zero, nullptr, 0,
-                          false, s));
-  CR_TRY(cr::compose_bias<T>(src("b_tok"), src("w_fuse") + (int64_t)dc * db, db, src("b_fuse"),
-                             reinterpret_cast<float*>(out + p.b_fuse), db, db, s));
+  for (int v = 0; v < 2; ++v) {
+    const bool rjv = v == 1;
+    if (rjv && d->n_blocks == 0) break;
+    T* wf = reinterpret_cast<T*>(out + (rjv ? p.w_fuse_rj : p.w_fuse));
+    CR_TRY(cr::transpose_into<T>(src("w_fuse"), rjv ? src("blk0.w_inj") : nullptr, wf, dc + E, dc,
+                                 db, s));
+    CR_TRY(cr::gemm_bias<T>(wft, db, src("w_tok"), db, db, E, db, wf + dc, dc + E, zero, nullptr,
+                            0, false, s));
+    CR_TRY(cr::compose_bias<T>(src("b_tok"), wfuse_t, db, src("b_fuse"),
+                               rjv ? src("blk0.b_inj") : nullptr,
+                               reinterpret_cast<float*>(out + (rjv ? p.b_fuse_rj : p.b_fuse)), db,
+                               db, s));
+  }
   for (int b = 0; b < d->n_blocks; ++b) {
     const std::string q = "blk" + std::to_string(b) + ".";
     const BlockP B = p.blk(b);
-    CR_TRY(mat(q + "w_inj", p.w_inj + (uint64_t)b * db * dc * sizeof(T), dc, db, dc));
-    CR_TRY(vec(q + "b_inj", p.b_inj + (uint64_t)b * db * 4, db));
     CR_TRY(vec(q + "ln1_g", B.ln1_g, db));
     CR_TRY(vec(q + "ln1_b", B.ln1_b, db));
     CR_TRY(mat(q + "w_qkv", B.w_qkv, db, 3 * db, db));
@@ -462,8 +473,19 @@ cr_status prepare_impl(const cr_dims* d, const cr_kv_layout* l, const char* blob
     CR_TRY(vec(q + "ln2_b", B.ln2_b, db));
     CR_TRY(mat(q + "w_ff1", B.w_ff1, db, r * db, db));
     CR_TRY(vec(q + "b_ff1", B.b_ff1, r * db));
-    CR_TRY(mat(q + "w_ff2", B.w_ff2, r * db, db, r * db));
+    // FFN2 rows [W_ff2 | W_inj_{b+1}] (zeros after the last block), biases
+    // b_ff2 and b_ff2 + b_inj_{b+1}
+    CR_TRY(mat(q + "w_ff2", B.w_ff2, r * db, db, r * db + dc));
     CR_TRY(vec(q + "b_ff2", B.b_ff2, db));
+    const std::string nq = "blk" + std::to_string(b + 1) + ".";
+    const bool has_next = b + 1 < d->n_blocks;
+    if (has_next)
+      CR_TRY(cr::transpose_into<T>(src(nq + "w_inj"), nullptr,
+                                   reinterpret_cast<T*>(out + B.w_ff2) + (int64_t)r * db,
+                                   r * db + dc, dc, db, s));
+    CR_TRY(cr::compose_bias<T>(nullptr, nullptr, 0, src(q + "b_ff2"),
+                               has_next ? src(nq + "b_inj") : nullptr,
+                               reinterpret_cast<float*>(out + B.b_ff2_rj), 0, db, s));
   }
   CR_TRY(vec("ln_f_g", p.ln_f_g, db));
   CR_TRY(vec("ln_f_b", p.ln_f_b, db));
@@ -511,9 +533,8 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
   int* flags = opt.keep_first ? reinterpret_cast<int*>(ws + W.flags) : nullptr;
   float2* rope = reinterpret_cast<float2*>(ws + W.rope);
   float2* krope = reinterpret_cast<float2*>(ws + W.krope);
-  T *U = WT(W.U), *st = WT(W.st), *inj = WT(W.inj), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q),
+  T *U = WT(W.U), *st = WT(W.st), *h = WT(W.h), *a = WT(W.a), *q = WT(W.q),
     *k = WT(W.k), *vt = WT(W.vt), *o = WT(W.o), *f = WT(W.f);
-  const int64_t ldinj = W.ldinj;
   const int B = d->n_blocks;
   cr::KvStrides ks{l->stride_layer, l->stride_kv, l->stride_token, l->stride_head,
                    l->n_kv_heads, l->head_dim};
@@ -561,22 +582,20 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
                           PF(P.b_cmp), nullptr, 0, false, s); }));
   CR_TRY(timed("layernorm", s, [&] {
       return cr::layernorm<T>(st, ldst, st, ldst, PF(P.ln_enc_g), PF(P.ln_enc_b), M, dc, eps, s); }));
-  // reinjection P_b(s) + b_b of every block at once -> inj[:, b*d_b : (b+1)*d_b]
-  // (none for the entrance-only variant)
+  // reinjections P_b(s) (none for the entrance-only variant) ride on the
+  // products before them: block 0's on the fusion, block b's on block b-1's
+  // FFN2 (extra K columns of s)
   const bool rj = opt.reinject && B > 0;
-  if (rj)
-    CR_TRY(timed("gemm_inject", s, [&] {
-        return cr::gemm_bias<T>(st, ldst, PT(P.w_inj), dc, M, B * db, dc, inj, ldinj,
-                                PF(P.b_inj), nullptr, 0, false, s); }));
-  // token projection and fusion as one product of [s ; e] -> h^0, plus
-  // block 0's reinjection
+  // token projection and fusion as one product of [s ; e] -> h^0 (+ P_0(s))
   CR_TRY(timed("gemm_fuse", s, [&] {
-      return cr::gemm_bias_split<T>(st, ldst, dc, emb, E, PT(P.w_fuse), dc + E, M, db, dc + E, h, db,
-                                    PF(P.b_fuse), rj ? inj : nullptr, ldinj, s); }));
+      return cr::gemm_bias_split<T>(st, ldst, dc, emb, E, PT(rj ? P.w_fuse_rj : P.w_fuse), dc + E,
+                                    M, db, dc + E, h, db, PF(rj ? P.b_fuse_rj : P.b_fuse), nullptr,
+                                    0, s); }));
   // h holds x_b = h^{b-1} + P_b(s) on entry to block b, h^B after the last block
+  const int kff = r * db;   // FFN2 inner width; its prepared rows are kff + d_c long
   for (int b = 0; b < B; ++b) {
     const BlockP Bk = P.blk(b);
-    const T* next_inj = rj && b + 1 < B ? inj + (int64_t)(b + 1) * db : nullptr;
+    const bool next_rj = rj && b + 1 < B;
     CR_TRY(timed("layernorm", s, [&] {
         return cr::layernorm<T>(h, db, a, db, PF(Bk.ln1_g), PF(Bk.ln1_b), M, db, eps, s); }));
     CR_TRY(timed("gemm_qkv", s, [&] {
@@ -592,8 +611,11 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
         return cr::gemm_bias<T>(a, db, PT(Bk.w_ff1), db, M, r * db, db, f, (int64_t)r * db,
                             PF(Bk.b_ff1), nullptr, 0, true, s); }));
     CR_TRY(timed("gemm_ffn2", s, [&] {
-        return cr::gemm_bias<T>(f, (int64_t)r * db, PT(Bk.w_ff2), (int64_t)r * db, M, db, r * db, h,
-                            db, PF(Bk.b_ff2), h, db, false, s, next_inj, ldinj); }));
+        if (next_rj)   // h^{b+1} + P_{b+1}(s) = h + [f ; s] [W_ff2 ; W_inj] + b_ff2 + b_inj
+          return cr::gemm_bias_split<T>(f, kff, kff, st, ldst, PT(Bk.w_ff2), kff + dc, M, db,
+                                        kff + dc, h, db, PF(Bk.b_ff2_rj), h, db, s);
+        return cr::gemm_bias<T>(f, kff, PT(Bk.w_ff2), kff + dc, M, db, kff, h, db, PF(Bk.b_ff2), h,
+                                db, false, s); }));
   }
   CR_TRY(timed("layernorm", s, [&] {
       return cr::layernorm<T>(h, db, a, db, PF(P.ln_f_g), PF(P.ln_f_b), M, db, eps, s); }));

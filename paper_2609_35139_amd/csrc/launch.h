@@ -136,10 +136,17 @@ hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* t
 hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s);
 
 // ---- weight preparation
-// out[n] = add[n] + sum_k v[k] * W[k][n] (W row-major [K][ldw]), in fp32.
+// out[n] = add[n] (+ add2[n]) + sum_k v[k] * W[k][n] (W row-major [K][ldw]),
+// in fp32; K may be 0.
 template <typename T>
-hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, float* out, int K,
-                        int N, hipStream_t s);
+hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, const T* add2,
+                        float* out, int K, int N, hipStream_t s);
+// dst[c][r] = src[r][c] (+ src2[r][c]) for r < R, c < C, summed in fp32 and
+// rounded once; dst rows are ldd apart and only their first R entries are
+// written (a block inside a wider prepared matrix).
+template <typename T>
+hipError_t transpose_into(const T* src, const T* src2, T* dst, int64_t ldd, int R, int C,
+                          hipStream_t s);
 // dst[b][c][r] = src[b][r][c] / div[b][r] for r < R, c < C; zero for
 // r in [R, ld_dst) and c in [C, Cp).
 template <typename Tin, typename Tout>

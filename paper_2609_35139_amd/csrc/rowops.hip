@@ -431,25 +431,50 @@ hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double the
 }
 
 // ------------------------------------------------------- weight preparation
-// Bias of two composed affine maps: out[n] = add[n] + sum_k v[k] W[k][n].
+// Bias of composed affine maps: out[n] = add[n] (+ add2[n]) + sum_k v[k] W[k][n].
 template <typename T>
 __global__ __launch_bounds__(256) void compose_bias_kernel(const T* __restrict__ v,
                                                            const T* __restrict__ W, int64_t ldw,
                                                            const T* __restrict__ add,
+                                                           const T* __restrict__ add2,
                                                            float* __restrict__ out, int K, int N) {
   const int n = blockIdx.x * 256 + threadIdx.x;
   if (n >= N) return;
   float acc = to_f32(add[n]);
+  if (add2) acc += to_f32(add2[n]);
   for (int k = 0; k < K; ++k) acc = fmaf(to_f32(v[k]), to_f32(W[(int64_t)k * ldw + n]), acc);
   out[n] = acc;
 }
 
 template <typename T>
-hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, float* out, int K,
-                        int N, hipStream_t s) {
+hipError_t compose_bias(const T* v, const T* W, int64_t ldw, const T* add, const T* add2,
+                        float* out, int K, int N, hipStream_t s) {
   if (N <= 0) return hipSuccess;
-  CR_LAUNCH((compose_bias_kernel<T>), dim3((N + 255) / 256), dim3(256), 0, s, v, W, ldw, add, out,
-            K, N);
+  CR_LAUNCH((compose_bias_kernel<T>), dim3((N + 255) / 256), dim3(256), 0, s, v, W, ldw, add, add2,
+            out, K, N);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_into_kernel(const T* __restrict__ src,
+                                                             const T* __restrict__ src2,
+                                                             T* __restrict__ dst, int64_t ldd,
+                                                             int R, int C) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)R * C) return;
+  const int c = (int)(idx / R), r = (int)(idx % R);
+  float v = to_f32(src[(int64_t)r * C + c]);
+  if (src2) v += to_f32(src2[(int64_t)r * C + c]);
+  dst[(int64_t)c * ldd + r] = from_f32<T>(v);
+}
+
+template <typename T>
+hipError_t transpose_into(const T* src, const T* src2, T* dst, int64_t ldd, int R, int C,
+                          hipStream_t s) {
+  const int64_t n = (int64_t)R * C;
+  if (n <= 0) return hipSuccess;
+  CR_LAUNCH((transpose_into_kernel<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src,
+            src2, dst, ldd, R, C);
   return hipGetLastError();
 }
 
@@ -510,8 +535,9 @@ hipError_t convert_f32(const Tin* src, float* dst, int64_t n, int64_t n_pad, int
                                               const float*, hipStream_t);                       \
   template hipError_t convert_f32<T>(const T*, float*, int64_t, int64_t, int, int64_t, int64_t, \
                                      hipStream_t);                                              \
-  template hipError_t compose_bias<T>(const T*, const T*, int64_t, const T*, float*, int, int,  \
-                                      hipStream_t);
+  template hipError_t compose_bias<T>(const T*, const T*, int64_t, const T*, const T*, float*,  \
+                                      int, int, hipStream_t);                                   \
+  template hipError_t transpose_into<T>(const T*, const T*, T*, int64_t, int, int, hipStream_t);
 CR_INST(bf16)
 CR_INST(float)
 #undef CR_INST

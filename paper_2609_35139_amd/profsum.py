@@ -45,7 +45,7 @@ CLASS_KERNEL = {
     "gemm_expand": ("EpiExpand", ["gemm.hip", "common.h", "launch.h"]),
     "gemm_qkv": ("EpiQKVh", ["gemm.hip", "common.h", "launch.h"]),
 }
-for _c in ("gemm_compress", "gemm_fuse", "gemm_inject", "gemm_oproj", "gemm_ffn1", "gemm_ffn2"):
+for _c in ("gemm_compress", "gemm_fuse", "gemm_oproj", "gemm_ffn1", "gemm_ffn2"):
     CLASS_KERNEL[_c] = ("EpiBias", ["gemm.hip", "common.h", "launch.h"])
 # the bench's 8192^3 bf16 library GEMM (measured-peak reference; no sources here)
 CLASS_KERNEL["library_gemm_8192"] = ("Cijk_", [])
@@ -119,7 +119,7 @@ def _per_dispatch(path, counter):
 
 def gemm_sequence(n_blocks):
     """Classes of the bias-epilogue GEMMs of one repair, in launch order."""
-    return (["gemm_compress", "gemm_inject", "gemm_fuse"] +
+    return (["gemm_compress", "gemm_fuse"] +
             ["gemm_oproj", "gemm_ffn1", "gemm_ffn2"] * n_blocks)
 
 

@@ -28,7 +28,12 @@ hipError_t gemm_bias_split(const T*, int64_t, int, const T*, int64_t, const T*, 
   return hipErrorInvalidValue;
 }
 template <typename T>
-hipError_t compose_bias(const T*, const T*, int64_t, const T*, float*, int, int, hipStream_t) {
+hipError_t compose_bias(const T*, const T*, int64_t, const T*, const T*, float*, int, int,
+                        hipStream_t) {
+  return hipErrorInvalidValue;
+}
+template <typename T>
+hipError_t transpose_into(const T*, const T*, T*, int64_t, int, int, hipStream_t) {
   return hipErrorInvalidValue;
 }
 template <typename T>
@@ -77,8 +82,9 @@ hipError_t convert_f32(const Tin*, float*, int64_t, int64_t, int, int64_t, int64
   template hipError_t gemm_bias_split<T>(const T*, int64_t, int, const T*, int64_t, const T*,   \
                                          int64_t, int, int, int, T*, int64_t, const float*,      \
                                          const T*, int64_t, hipStream_t);                        \
-  template hipError_t compose_bias<T>(const T*, const T*, int64_t, const T*, float*, int, int,   \
-                                      hipStream_t);                                              \
+  template hipError_t compose_bias<T>(const T*, const T*, int64_t, const T*, const T*, float*,  \
+                                      int, int, hipStream_t);                                    \
+  template hipError_t transpose_into<T>(const T*, const T*, T*, int64_t, int, int, hipStream_t); \
   template hipError_t gemm_qkv<T>(const T*, int64_t, const T*, int, int, int, int, T*, T*, T*,   \
                                   int64_t, const float*, const float2*, hipStream_t);             \
   template hipError_t gemm_expand<T>(const T*, int64_t, const T*, int, int, int, T*, KvStrides,   \

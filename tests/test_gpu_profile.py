@@ -27,7 +27,7 @@ def _cuda():
 def _expected(n_blocks):
     """(class, launches) of a method repair with reinjection, in first-launch order."""
     return [("schedule", 1), ("rope_table", 1), ("compress_segments", 1), ("gemm_compress", 1),
-            ("layernorm", 2 * n_blocks + 2), ("gemm_inject", 1), ("gemm_fuse", 1),
+            ("layernorm", 2 * n_blocks + 2), ("gemm_fuse", 1),
             ("gemm_qkv", n_blocks), ("attention", n_blocks),
             ("gemm_oproj", n_blocks), ("gemm_ffn1", n_blocks), ("gemm_ffn2", n_blocks),
             ("gemm_expand", 1)]
