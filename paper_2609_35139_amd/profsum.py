@@ -43,7 +43,7 @@ CLASS_KERNEL = {
     "layernorm": ("layernorm_kernel", ["rowops.hip", "common.h", "launch.h"]),
     "compress_segments": ("compress_segments_kernel", ["rowops.hip", "common.h", "launch.h"]),
     "gemm_expand": ("EpiExpand", ["gemm.hip", "common.h", "launch.h"]),
-    "gemm_qkv": ("EpiQKVh", ["gemm.hip", "common.h", "launch.h"]),
+    "gemm_qkv": ("EpiQKV", ["gemm.hip", "common.h", "launch.h"]),   # EpiQKVh or EpiQKV
 }
 for _c in ("gemm_compress", "gemm_fuse", "gemm_oproj", "gemm_ffn1", "gemm_ffn2"):
     CLASS_KERNEL[_c] = ("EpiBias", ["gemm.hip", "common.h", "launch.h"])
@@ -87,6 +87,19 @@ def kernel_stats(stats_csv, bench_json, command):
         out.append("%-36s %8s %12.1f %10.2f %7.2f" % (
             short_name(r["Name"]), r["Calls"], float(r["TotalDurationNs"]) / 1e3,
             float(r["AverageNs"]) / 1e3, float(r["Percentage"])))
+    # per class from the kernel trace of the same run (classes by launch order)
+    trace = os.path.join(os.path.dirname(stats_csv), "run_kernel_trace.csv")
+    if os.path.exists(trace):
+        tr = sorted(csv.DictReader(open(trace)), key=lambda r: int(r["Dispatch_Id"]))
+        durs = {}
+        for r, cls in zip(tr, classify([r["Kernel_Name"] for r in tr], b)):
+            if cls:
+                durs.setdefault(cls, []).append(
+                    (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        out += ["", "# per-class average launch from the kernel trace of the same run (us;",
+                "# bias-epilogue GEMMs told apart by their place in the launch order):",
+                "#   " + ", ".join("%s %.2f (%d)" % (c, sum(v) / len(v), len(v))
+                                   for c, v in durs.items())]
     rf = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in b["roofline"].items()}
     out += ["", "# bench line of the same command (live HIP events on the library's stream):",
             "#   ms_per_step %.3f, value %.4g tokens/s" % (b["ms_per_step"], b["value"]),
@@ -128,16 +141,8 @@ def _class_values(path, counter, cls, bench):
     a bias epilogue share one device function; they are told apart by their
     position in the repair's fixed launch order (the profiled command runs
     nothing else that launches them)."""
-    sub = CLASS_KERNEL[cls][0]
-    ds = [(n, v) for _, n, v in _dispatches(path, counter) if sub in n]
-    if sub != "EpiBias":
-        return [v for _, v in ds]
-    per_step = {k["class"]: k["launches_per_step"] for k in bench["kernels"]}
-    seq = gemm_sequence(per_step.get("gemm_oproj", 0))
-    if len(ds) % len(seq):
-        raise ValueError(f"{len(ds)} bias-epilogue GEMM dispatches do not split into "
-                         f"repairs of {len(seq)}")
-    return [v for i, (_, v) in enumerate(ds) if seq[i % len(seq)] == cls]
+    ds = _dispatches(path, counter)
+    return [v for (_, _, v), c in zip(ds, classify([n for _, n, _ in ds], bench)) if c == cls]
 
 
 def _calibration(per_kernel, copy_bytes):
@@ -199,6 +204,28 @@ SQ_RATIOS = (
 )
 
 
+def classify(names, bench):
+    """Kernel class of each dispatch, given the dispatches' kernel names in
+    dispatch order (None for kernels of no class).  Bias-epilogue GEMMs share
+    device functions across classes and are assigned by their position in
+    the repair's fixed launch order, after the weight preparation's own
+    GEMMs (one or two, launched once before the first repair)."""
+    per_step = {k["class"]: k["launches_per_step"] for k in bench["kernels"]}
+    seq = gemm_sequence(per_step.get("gemm_oproj", 0))
+    skip = sum("EpiBias" in n for n in names) % len(seq)
+    out, k = [], 0
+    for name in names:
+        cls = None
+        for c, (sub, _) in CLASS_KERNEL.items():
+            if sub != "EpiBias" and sub in name and "EpiExpandRope" not in name:
+                cls = c
+        if "EpiBias" in name:
+            cls = seq[(k - skip) % len(seq)] if k >= skip else None
+            k += 1
+        out.append(cls)
+    return out
+
+
 def counters(csv_path, bench_json, command, n_cus=256):
     """Per-class means of one --pmc pass (one row per dispatch and counter)
     and the derived ratios of SQ_RATIOS."""
@@ -209,20 +236,11 @@ def counters(csv_path, bench_json, command, n_cus=256):
         e = disp.setdefault(d, {"name": r["Kernel_Name"],
                                 "dur_ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
         e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
-    per_step = {k["class"]: k["launches_per_step"] for k in b["kernels"]}
-    seq = gemm_sequence(per_step.get("gemm_oproj", 0))
-    by_cls, k = {}, 0
-    for d in sorted(disp):
-        e = disp[d]
-        cls = None
-        for c, (sub, _) in CLASS_KERNEL.items():
-            if sub != "EpiBias" and sub in e["name"] and "EpiExpandRope" not in e["name"]:
-                cls = c
-        if "EpiBias" in e["name"]:
-            cls = seq[k % len(seq)]
-            k += 1
+    order = sorted(disp)
+    by_cls = {}
+    for d, cls in zip(order, classify([disp[d]["name"] for d in order], b)):
         if cls:
-            by_cls.setdefault(cls, []).append(e)
+            by_cls.setdefault(cls, []).append(disp[d])
     names = sorted({n for e in disp.values() for n in e if n.isupper() or n.startswith("SQ_")})
     out = [f"# SQ counters per kernel class, workload {b['config']['workload']}",
            f"# command: {command}",
