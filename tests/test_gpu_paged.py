@@ -124,3 +124,38 @@ def test_paged_rotate_keys_is_bit_identical():
     got = W.kv_layer_major_to_canonical(gathered)
     assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 4e-6 * np.abs(X).max())
     assert np.array_equal(gathered, kv_a.float().cpu().numpy())
+
+
+def test_paged_and_out_of_place_at_the_4x256_workload():
+    """At the 4x256 workload (1,024 tokens, 18,432 cache columns: the
+    expansion's large-grid tiles, with a partly filled last row of tiles) a
+    paged cache repaired in place, and a contiguous cache repaired out of
+    place into a paged one, give the contiguous in-place result bit for bit."""
+    import torch
+    from paper_2609_35139_amd import binding as B
+    w = W.workload(1)
+    inp = W.make_inputs(w)
+    rep = repairer_for(w, inp.weights)
+    t = w.target
+    bs = 16
+    emb = to_device(w, inp.token_embeds)
+    kv_a = to_device(w, inp.kv)
+    rep.repair(kv_a, w.chunk_offsets, w.request_chunks, emb)
+    ref = kv_a.float().cpu().numpy()
+    pool, table = _pool(w, inp.kv.astype(np.float32), bs, 3, 29)
+    lay, sB = B.paged_layout(t.n_layers, t.n_kv_heads, t.head_dim, pool.shape[2], bs,
+                             B.CR_DTYPE_BF16)
+    pages = dict(block_size=bs, n_blocks=pool.shape[2], stride_block=sB, block_table=table)
+    kv_p = to_device(w, pool)
+    rep.repair(kv_p, w.chunk_offsets, w.request_chunks, emb, layout=lay,
+               workspace=rep.workspace(w.n_tokens), options=B.Options(pages=pages))
+    # out of place: contiguous source (left as it was), paged destination
+    kv_src = to_device(w, inp.kv)
+    kv_dst = to_device(w, np.full_like(pool, 7.5))
+    rep.repair(kv_src, w.chunk_offsets, w.request_chunks, emb,
+               workspace=rep.workspace(w.n_tokens),
+               options=B.Options(kv_out=kv_dst.data_ptr(), layout_out=lay, pages_out=pages))
+    torch.cuda.synchronize()
+    assert np.array_equal(_gather(kv_p.float().cpu().numpy(), table, w.n_tokens, bs), ref)
+    assert np.array_equal(_gather(kv_dst.float().cpu().numpy(), table, w.n_tokens, bs), ref)
+    assert np.array_equal(kv_src.float().cpu().numpy(), inp.kv.astype(np.float32))
