@@ -692,20 +692,28 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
     bsrc[r] = reinterpret_cast<const char*>(B + (int64_t)epi.b_row(min(n0 + row, N - 1)) * ldb) +
               chunk * 16;
   }
-  auto issue = [&](int kt, int stage) {
+  // DMA operation o (A rounds first, then B rounds) of slab kt into a stage
+  auto dma_op = [&](int o, int kt, int stage) {
     char* base = smem + stage * G::STAGE_BYTES;
-#pragma unroll
-    for (int r = 0; r < G::A_ROUNDS; ++r) {
-      const char* a = asrc[r] + kt * 128;
+    if (o < G::A_ROUNDS) {
+      const char* a = asrc[o] + kt * 128;
       if constexpr (SPLIT) {
-        if (kt >= kt1) a = asrc2[r] + (kt - kt1) * 128;
+        if (kt >= kt1) a = asrc2[o] + (kt - kt1) * 128;
       }
-      dma16(a, base + (r * G::NW + wave) * 1024);
-    }
-#pragma unroll
-    for (int r = 0; r < G::B_ROUNDS; ++r)
+      dma16(a, base + (o * G::NW + wave) * 1024);
+    } else {
+      const int r = o - G::A_ROUNDS;
       dma16(bsrc[r] + kt * 128, base + G::BM * 128 + (r * G::NW + wave) * 1024);
+    }
   };
+  auto issue = [&](int kt, int stage) {
+#pragma unroll
+    for (int o = 0; o < G::OPS; ++o) dma_op(o, kt, stage);
+  };
+  // Spread issue: every slab is loaded, past the end as a copy of the last
+  // slab into a stage nobody reads again, so each iteration issues the same
+  // OPS operations between its products and waits for the same count.
+  constexpr bool SPREAD = G::BM <= 128 && G::NW == 8;
 
   // the epilogue's global loads (bias, residuals, the stale cache) go out
   // before the main loop and land while it runs
@@ -723,15 +731,21 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 
   const int KT = K / G::BK;
 #pragma unroll
-  for (int st = 0; st < G::STAGES - 1; ++st)
-    if (st < KT) issue(st, st);
+  for (int st = 0; st < G::STAGES - 1; ++st) {
+    if constexpr (SPREAD) issue(min(st, KT - 1), st);
+    else if (st < KT) issue(st, st);
+  }
 
   // fragment rows: wm + i*32 + (lane & 31); all share swizzle ((lane & 15) >> 1)
   const int fr = lane & 31, fsw = (lane & 15) >> 1;
   for (int kt = 0; kt < KT; ++kt) {
-    wait_slab<G::OPS, G::STAGES - 2>(min(G::STAGES - 2, KT - 1 - kt));
+    if constexpr (SPREAD) wait_vmcnt<G::OPS * (G::STAGES - 2)>();
+    else wait_slab<G::OPS, G::STAGES - 2>(min(G::STAGES - 2, KT - 1 - kt));
     __builtin_amdgcn_s_barrier();
-    if (kt + G::STAGES - 1 < KT) issue(kt + G::STAGES - 1, (kt + G::STAGES - 1) % G::STAGES);
+    const int nkt = min(kt + G::STAGES - 1, KT - 1), nst = (kt + G::STAGES - 1) % G::STAGES;
+    if constexpr (!SPREAD) {
+      if (kt + G::STAGES - 1 < KT) issue(nkt, nst);
+    }
 
     const char* as = smem + (kt % G::STAGES) * G::STAGE_BYTES;
     const char* bs = as + G::BM * 128;
@@ -759,9 +773,13 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 #pragma unroll
         for (int j = 0; j < G::TN; ++j)
           acc[i][j] = MM::mma(bfr[ks & 1][j], af[ks & 1][i], acc[i][j]);
+      if constexpr (SPREAD) {
+        if (ks == NKS - 1) issue(nkt, nst);
+      }
     }
     // instruction order for the scheduler: the first step's LDS reads, then
-    // every step's MFMAs alternating with the next step's reads
+    // every step's MFMAs alternating with the next step's reads (and, spread,
+    // with its share of the next slab's DMA operations)
     constexpr int NR = G::TM + G::TN, NM = G::TM * G::TN;
     constexpr int NP = NR < NM ? NR : NM;
     __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);        // DS reads
@@ -775,8 +793,22 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
       if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
       if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    if constexpr (SPREAD) {
+      // the last step reads nothing, so its products carry the DMA issue
+      // (which, writing LDS, stays behind every fragment read before it)
+#pragma unroll
+      for (int r = 0; r < NM; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        constexpr int DQ = G::OPS / NM, DR = G::OPS % NM;
+        if (r < DR) __builtin_amdgcn_sched_group_barrier(0x020, DQ + 1, 0);
+        else if (DQ > 0) __builtin_amdgcn_sched_group_barrier(0x020, DQ > 0 ? DQ : 1, 0);
+      }
+    } else {
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    }
   }
+  // the copies past the last slab land in the ring, which the epilogue reuses
+  if constexpr (SPREAD) wait_vmcnt<0>();
 
   // Epilogue.  With the weight tile as the MFMA's first operand, lane l of
   // atom (i, j) holds output row wm + i*32 + (l & 31) and, in registers
