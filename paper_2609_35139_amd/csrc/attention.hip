@@ -192,14 +192,11 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   auto step = [&](auto slot, int it) {
     constexpr int J = decltype(slot)::value;
     if (it >= iters) return;
-    // this group's tile `it` has landed once min(STAGES-2, mine-1-it) later ones remain
-    const int ahead = min(C::STAGES - 2, mine - 1 - it);
-    if (C::STAGES >= 4 && ahead >= 2) wait_vmcnt<2 * C::OPS>();
-    else if (C::STAGES >= 3 && ahead >= 1) wait_vmcnt<C::OPS>();
-    else wait_vmcnt<0>();
+    // every iteration issues one tile (past the group's last tile, a copy of
+    // it into a slot nobody reads again), so tile `it` has landed once
+    // STAGES-2 later ones remain in flight
+    wait_vmcnt<(C::STAGES - 2) * C::OPS>();
     __builtin_amdgcn_s_barrier();   // the slot refilled below is no longer read by anyone
-    if (it + C::STAGES - 1 < mine)
-      issue(it + C::STAGES - 1, ((J + C::STAGES - 1) % C::STAGES) * C::STAGE_BYTES);
     if (it >= mine) return;         // group 1 without a last tile: only keeps the barrier count
     constexpr int SO = J * C::STAGE_BYTES;
     // the compiler's interleaving of LDS reads with MFMAs for this tile's
@@ -228,6 +225,10 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
             vf[rt][s2][d] = *reinterpret_cast<const frag*>(vp[rt][s2] + (SO + d * 32 * C::RBV));
     };
     if constexpr (kEarlyV) read_v();
+    // the refill of the slot freed by the barrier goes out after this tile's
+    // fragment reads (a DMA writes LDS, so the compiler keeps it behind every
+    // earlier read), among the score products instead of ahead of them
+    issue(min(it + C::STAGES - 1, mine - 1), ((J + C::STAGES - 1) % C::STAGES) * C::STAGE_BYTES);
     // the accumulators start at -m_use, so the scores arrive already shifted
     // by the row's reference max (no per-score subtraction)
     f32x16 s[2];
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
 
 #pragma unroll
   for (int st = 0; st < C::STAGES - 1; ++st)
-    if (st < mine) issue(st, st * C::STAGE_BYTES);
+    if (mine > 0) issue(min(st, mine - 1), st * C::STAGE_BYTES);
   for (int it0 = 0; it0 < iters; it0 += C::STAGES) {
     step(std::integral_constant<int, 0>{}, it0);
     step(std::integral_constant<int, 1>{}, it0 + 1);
@@ -328,6 +329,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
 
   // merge group 1 into group 0: per query q' = gw*32 + ql, lane half g holds
   // l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4 of O^T
+  wait_vmcnt<0>();   // the copies past the last tile land in the rings
   __syncthreads();   // both rings idle
   float* mo = reinterpret_cast<float*>(lds);                  // [BQ][MLD] O^T values
   float* ml = mo + C::BQ * C::MLD;                            // [BQ][2] (m, l) per lane half
