@@ -32,7 +32,7 @@ FUNCTION_OF = {
     "gemm_ffn2": "gemm_nt_kernel<EpiBias>", "gemm_qkv": "gemm_nt_kernel<EpiQKVh|EpiQKV>",
     "gemm_expand": "gemm_nt_kernel<EpiExpand>", "attention": "attention_kernel",
     "layernorm": "layernorm_kernel", "compress_segments": "compress_segments_kernel",
-    "schedule": "schedule_kernel", "rope_table": "rope_table_kernel",
+    "schedule": "schedule_kernel",
 }
 
 

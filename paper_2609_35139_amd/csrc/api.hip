@@ -565,11 +565,10 @@ cr_status repair_impl(T* kv, const cr_kv_layout* l, const int32_t* off, int32_t 
     }
   }
 
+  // the schedule also writes the repair network's RoPE table of the positions
   CR_TRY(timed("schedule", s, [&] {
       return cr::chunk_schedule(off, n_chunks, req, n_req, opt.mask, opt.pos_offset, lo, hi, pos,
-                                gpos, flags, s); }));
-  CR_TRY(timed("rope_table", s, [&] {
-      return cr::rope_table(rope, pos, (int)M, dhd, (double)d->rope_theta, s); }));
+                                gpos, flags, s, rope, dhd, (double)d->rope_theta); }));
   if (opt.place_keys)
     CR_TRY(timed("key_rope_table", s, [&] {
         return cr::key_rope_table(krope, gpos, M, opt.kr, s); }));

@@ -110,11 +110,14 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
 // ---- chunk schedule: per token the key interval [lo, hi) of the attention
 // topology `mask` (values of CR_MASK_*), the position within the request and,
 // when the pointers are not null, the global position (position_offset of the
-// request + position; pos_offset may be null = 0) and the first-chunk flag.
+// request + position; pos_offset may be null = 0), the first-chunk flag and
+// the RoPE (cos, sin) row of the position: rope[t][i] = (cos, sin)(pos[t] *
+// theta^(-2i / d_head)), i < d_head / 2, computed in fp64.
 hipError_t chunk_schedule(const int32_t* chunk_offsets, int32_t n_chunks,
                           const int32_t* request_chunks, int32_t n_requests, int mask,
                           const int32_t* pos_offset, int* lo, int* hi, int* pos, int* gpos,
-                          int* flags, hipStream_t s);
+                          int* flags, hipStream_t s, float2* rope = nullptr, int d_head = 0,
+                          double theta = 0.0);
 
 // ---- target-model key rotation R_M(p): frequencies of the rotate-half pairs
 // (fp64) and the factor applied to cos and sin.
@@ -130,10 +133,6 @@ hipError_t key_rope_table(float2* tab, const int* gpos, int N, const KeyRope& kr
 template <typename T>
 hipError_t rotate_keys(T* kv, KvStrides ks, int n_layers, int N, const float2* tab, bool inverse,
                        float scale, hipStream_t s);
-
-// ---- RoPE (cos, sin) table per token: tab[t][i] = (cos, sin)(pos[t] * f_i),
-// f_i = theta^(-2i / d_head), i < d_head / 2, computed in fp64.
-hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s);
 
 // ---- weight preparation
 // out[n] = add[n] (+ add2[n]) + sum_k v[k] * W[k][n] (W row-major [K][ldw]),

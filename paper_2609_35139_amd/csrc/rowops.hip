@@ -229,7 +229,11 @@ hipError_t compress_segments(const T* kv, KvStrides ks, int n_layers, const T* w
 // Per token t: the key interval [lo, hi) of its attention row under the
 // chosen topology (all of them allow only t's request), its 0-based position
 // within the request, optionally its global position and a flag for the
-// first chunk of its request.  Chunks are passed by value in batches.
+// first chunk of its request, and optionally the repair network's RoPE row
+// of that position (one row per token, so that the QKV epilogue's table
+// reads do not wait for a position load first).  Chunks are passed by value
+// in batches.  With the table, thread (t, i) handles pair i of token t and
+// the threads with i = 0 write the schedule.
 constexpr int SCHED_CHUNKS = 128;
 struct SchedBatch {
   int count;                          // chunks in this batch
@@ -241,12 +245,20 @@ struct SchedBatch {
   unsigned first[SCHED_CHUNKS / 32];  // bit c: chunk c opens its request
 };
 
+struct RopeRow {
+  float2* tab;     // [token][half] (cos, sin), or null
+  int half;        // d_head / 2 (1 without a table)
+  int d_head;
+  double theta;
+};
+
 __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __restrict__ lo,
                                                        int* __restrict__ hi,
                                                        int* __restrict__ pos,
                                                        int* __restrict__ gpos,
-                                                       int* __restrict__ flags) {
-  const int t = sb.offs[0] + blockIdx.x * 256 + threadIdx.x;
+                                                       int* __restrict__ flags, RopeRow rr) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int t = sb.offs[0] + (int)(idx / rr.half), i = (int)(idx % rr.half);
   if (t >= sb.offs[sb.count]) return;
   // largest c with offs[c] <= t (skips empty chunks)
   int a = 0, b = sb.count;
@@ -258,16 +270,27 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __res
   if (sb.mask == 1) h = t + 1;                      // token-causal: j <= i
   else if (sb.mask == 2) h = sb.req_end[a];         // bidirectional
   else if (sb.mask == 3) l = sb.offs[a];            // block-diagonal: c(j) == c(i)
-  lo[t] = l;
-  hi[t] = h;
-  pos[t] = t - sb.req_start[a];
-  if (gpos) gpos[t] = t + sb.gbase[a];
-  if (flags) flags[t] = (sb.first[a >> 5] >> (a & 31)) & 1;
+  const int p = t - sb.req_start[a];
+  if (i == 0) {
+    lo[t] = l;
+    hi[t] = h;
+    pos[t] = p;
+    if (gpos) gpos[t] = t + sb.gbase[a];
+    if (flags) flags[t] = (sb.first[a >> 5] >> (a & 31)) & 1;
+  }
+  // (cos, sin)(p * theta^(-2i / d_head)), angle and cosines in fp64
+  if (rr.tab) {
+    const double ang = (double)p * pow(rr.theta, -2.0 * (double)i / (double)rr.d_head);
+    rr.tab[(int64_t)t * rr.half + i] = make_float2((float)cos(ang), (float)sin(ang));
+  }
 }
 
 hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* req,
                           int32_t n_req, int mask, const int32_t* pos_offset, int* lo, int* hi,
-                          int* pos, int* gpos, int* flags, hipStream_t s) {
+                          int* pos, int* gpos, int* flags, hipStream_t s, float2* rope,
+                          int d_head, double theta) {
+  RopeRow rr{rope, rope ? d_head / 2 : 1, d_head, theta};
+  if (rope && rr.half < 1) return hipErrorInvalidValue;
   std::vector<int> rs(n_chunks), re(n_chunks), gb(n_chunks), first(n_chunks);
   const int nr = req ? n_req : 1;
   for (int r = 0; r < nr; ++r) {
@@ -293,8 +316,9 @@ hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* r
     }
     const int ntok = sb.offs[sb.count] - sb.offs[0];
     if (ntok == 0) continue;
-    CR_LAUNCH(schedule_kernel, dim3((ntok + 255) / 256), dim3(256), 0, s, sb, lo, hi, pos, gpos,
-              flags);
+    const int64_t nthr = (int64_t)ntok * rr.half;
+    CR_LAUNCH(schedule_kernel, dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, s, sb, lo, hi,
+              pos, gpos, flags, rr);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -407,28 +431,6 @@ template hipError_t rotate_keys<bf16>(bf16*, KvStrides, int, int, const float2*,
                                       hipStream_t);
 template hipError_t rotate_keys<float>(float*, KvStrides, int, int, const float2*, bool, float,
                                        hipStream_t);
-
-// ------------------------------------------------------------ RoPE table
-// One row per token, so that the QKV epilogue's table reads do not wait for
-// a position load first.
-__global__ __launch_bounds__(256) void rope_table_kernel(float2* __restrict__ tab,
-                                                         const int* __restrict__ pos, int N,
-                                                         int half, int d_head, double theta) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)N * half) return;
-  const int t = (int)(idx / half), i = (int)(idx % half);
-  const double ang = (double)pos[t] * pow(theta, -2.0 * (double)i / (double)d_head);
-  tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
-}
-
-hipError_t rope_table(float2* tab, const int* pos, int N, int d_head, double theta, hipStream_t s) {
-  const int half = d_head / 2;
-  const int64_t n = (int64_t)N * half;
-  if (n <= 0) return hipSuccess;
-  CR_LAUNCH(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tab, pos, N,
-            half, d_head, theta);
-  return hipGetLastError();
-}
 
 // ------------------------------------------------------- weight preparation
 // Bias of composed affine maps: out[n] = add[n] (+ add2[n]) + sum_k v[k] W[k][n].

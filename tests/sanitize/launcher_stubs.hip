@@ -7,13 +7,10 @@ namespace cr {
 
 hipError_t copy_table(const int32_t*, int, int*, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t chunk_schedule(const int32_t*, int32_t, const int32_t*, int32_t, int, const int32_t*,
-                          int*, int*, int*, int*, int*, hipStream_t) {
+                          int*, int*, int*, int*, int*, hipStream_t, float2*, int, double) {
   return hipErrorInvalidValue;
 }
 hipError_t key_rope_table(float2*, const int*, int, const KeyRope&, hipStream_t) {
-  return hipErrorInvalidValue;
-}
-hipError_t rope_table(float2*, const int*, int, int, double, hipStream_t) {
   return hipErrorInvalidValue;
 }
 

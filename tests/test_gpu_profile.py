@@ -26,7 +26,7 @@ def _cuda():
 
 def _expected(n_blocks):
     """(class, launches) of a method repair with reinjection, in first-launch order."""
-    return [("schedule", 1), ("rope_table", 1), ("compress_segments", 1), ("gemm_compress", 1),
+    return [("schedule", 1), ("compress_segments", 1), ("gemm_compress", 1),
             ("layernorm", 2 * n_blocks + 2), ("gemm_fuse", 1),
             ("gemm_qkv", n_blocks), ("attention", n_blocks),
             ("gemm_oproj", n_blocks), ("gemm_ffn1", n_blocks), ("gemm_ffn2", n_blocks),
@@ -68,8 +68,8 @@ def test_profiled_repair_counts_classes_and_matches_unprofiled(dtype, n_blocks):
     rep.repair(kv, w.chunk_offsets, w.request_chunks, emb, workspace=ws)
     stats = B.cr_profile_read()
     assert [(s["name"], s["launches"]) for s in stats] == [
-        ("schedule", 1), ("rope_table", 1), ("compress_segments", 1), ("gemm_compress", 1),
-        ("layernorm", 1)]
+        ("schedule", 1), ("compress_segments", 1), ("gemm_compress", 1),
+        ("layernorm", 1), ("gemm_fuse", 1)]
     assert torch.equal(kv, ref)
 
     # disabled: nothing is recorded

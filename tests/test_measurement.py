@@ -63,7 +63,7 @@ def _repair_names(n_blocks):
     """Kernel names of one repair's dispatches in launch order (method, with
     reinjection), as the device functions are named."""
     bias = "void cr::gemm_nt_kernel<bf16, Tile, cr::EpiBias<bf16>, false>(...)"
-    out = ["cr::schedule_kernel", "cr::rope_table_kernel", "cr::compress_segments_kernel<...>",
+    out = ["cr::schedule_kernel", "cr::compress_segments_kernel<...>",
            bias, "cr::layernorm_kernel<...>", bias]
     for _ in range(n_blocks):
         out += ["cr::layernorm_kernel<...>", "void cr::gemm_nt_kernel<bf16, T, cr::EpiQKVh<bf16>>",
@@ -84,7 +84,7 @@ def test_classify_skips_the_preparation_gemms_and_follows_launch_order():
     cls = profsum.classify(names, _bench_stub(B))
     assert cls[:4] == [None] * 4
     one = cls[4:4 + len(_repair_names(B))]
-    expect = ["schedule", "rope_table", "compress_segments", "gemm_compress", "layernorm",
+    expect = ["schedule", "compress_segments", "gemm_compress", "layernorm",
               "gemm_fuse"]
     for _ in range(B):
         expect += ["layernorm", "gemm_qkv", "attention", "gemm_oproj", "layernorm", "gemm_ffn1",
