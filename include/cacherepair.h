@@ -442,9 +442,9 @@ CR_API cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layo
  * hipMalloc, harnesses without an allocator.  Same arguments as cr_repair
  * minus the workspace; same kernels and bit-identical results.  The
  * workspace is a device array inside the library of CR_STATIC_SCRATCH_BYTES
- * bytes (192 MiB: enough for a 4,096-token request of a Qwen2.5-3B-shaped
- * cache with a d_b = 1024, 8-block repairer), held by every GPU the library
- * runs on until the process ends.  A call needing more (see
+ * bytes (128 MiB: enough for a 4,096-token request of a Qwen2.5-3B-shaped
+ * cache with a d_b = 1024, 8-block repairer, which needs 118.1 MiB), held by
+ * every GPU the library runs on until the process ends.  A call needing more (see
  * cr_workspace_bytes) returns CR_ERR_WORKSPACE before anything is enqueued.
  * The call allocates nothing, on the host or the device.  Every call on one
  * GPU uses that GPU's one array, which keeps the previous call's contents
@@ -453,7 +453,7 @@ CR_API cr_status cr_workspace_view(const cr_dims* dims, const cr_kv_layout* layo
  * e.g. on one stream.  Errors as cr_repair; CR_ERR_DEVICE also when the
  * array's device address cannot be obtained.
  */
-#define CR_STATIC_SCRATCH_BYTES (192ull << 20)
+#define CR_STATIC_SCRATCH_BYTES (128ull << 20)
 CR_API cr_status cr_repair_static(void* kv, const cr_kv_layout* layout,
                                   const int32_t* chunk_offsets, int32_t n_chunks,
                                   const int32_t* request_chunks, int32_t n_requests,

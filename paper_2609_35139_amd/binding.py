@@ -33,7 +33,7 @@ EXPORTS = ["cr_version", "cr_status_string", "cr_weights_layout", "cr_prepared_b
            "cr_pipeline_create", "cr_pipeline_destroy", "cr_pipeline_staging_bytes",
            "cr_repair_pipelined", "cr_workspace_view", "cr_profile_enable", "cr_profile_read",
            "cr_repair_static"]
-CR_STATIC_SCRATCH_BYTES = 192 << 20
+CR_STATIC_SCRATCH_BYTES = 128 << 20
 CR_MASK = {"block_causal": 0, "token_causal": 1, "bidirectional": 2, "block_diagonal": 3}
 CR_APPLY = {"kv": 0, "k": 1, "v": 2}
 

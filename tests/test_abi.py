@@ -370,7 +370,7 @@ def test_pipeline_validation():
 def test_static_scratch_entry_point_validates_on_the_host():
     """cr_repair_static rejects a NULL cache and a workspace need beyond
     CR_STATIC_SCRATCH_BYTES before touching any device."""
-    w = W.WORKLOADS[3]                     # 10 x 512 Llama-3-8B-shaped: needs > 192 MiB
+    w = W.WORKLOADS[3]                     # 10 x 512 Llama-3-8B-shaped: needs > 128 MiB
     dims, lay = _dims(w), _layout(w)
     assert B.cr_workspace_bytes(dims, lay, w.n_tokens) > B.CR_STATIC_SCRATCH_BYTES
     prep_bytes = B.cr_prepared_bytes(dims, lay)
