@@ -710,9 +710,13 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 #pragma unroll
     for (int o = 0; o < G::OPS; ++o) dma_op(o, kt, stage);
   };
-  // Spread issue: every slab is loaded, past the end as a copy of the last
-  // slab into a stage nobody reads again, so each iteration issues the same
-  // OPS operations between its products and waits for the same count.
+  // Spread issue (the 8-wave 128-row tiles, whose 4-slab rings give a refill
+  // three iterations to land): the refill goes out between the products of
+  // the slab's last k-step instead of as a burst after the barrier.  Every
+  // slab is loaded, past the end as a copy of the last slab into a stage
+  // nobody reads again, so each iteration issues the same OPS operations and
+  // waits for the same count.  (2-slab rings keep the burst: their refill
+  // must land within the iteration.)
   constexpr bool SPREAD = G::BM <= 128 && G::NW == 8;
 
   // the epilogue's global loads (bias, residuals, the stale cache) go out
@@ -799,9 +803,9 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
 #pragma unroll
       for (int r = 0; r < NM; ++r) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        constexpr int DQ = G::OPS / NM, DR = G::OPS % NM;
+        constexpr int DQ = G::OPS / NM, DR = G::OPS % NM;   // DMA ops per product
         if (r < DR) __builtin_amdgcn_sched_group_barrier(0x020, DQ + 1, 0);
-        else if (DQ > 0) __builtin_amdgcn_sched_group_barrier(0x020, DQ > 0 ? DQ : 1, 0);
+        else if constexpr (DQ > 0) __builtin_amdgcn_sched_group_barrier(0x020, DQ, 0);
       }
     } else {
       __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
