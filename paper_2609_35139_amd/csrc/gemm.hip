@@ -711,8 +711,11 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
     for (int o = 0; o < G::OPS; ++o) dma_op(o, kt, stage);
   };
   // Spread issue (the 8-wave 128-row tiles, whose 4-slab rings give a refill
-  // three iterations to land): the refill goes out between the products of
-  // the slab's last k-step instead of as a burst after the barrier.  Every
+  // three iterations to land): the refill goes out in equal shares over the
+  // slab's k-steps, each share after that step's fragment reads for the next
+  // step (a DMA writes LDS, so the compiler keeps it behind every earlier
+  // read) and among its products, instead of as a burst after the barrier.
+  // Every
   // slab is loaded, past the end as a copy of the last slab into a stage
   // nobody reads again, so each iteration issues the same OPS operations and
   // waits for the same count.  (2-slab rings keep the burst: their refill
@@ -778,7 +781,9 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
         for (int j = 0; j < G::TN; ++j)
           acc[i][j] = MM::mma(bfr[ks & 1][j], af[ks & 1][i], acc[i][j]);
       if constexpr (SPREAD) {
-        if (ks == NKS - 1) issue(nkt, nst);
+        // this k-step's share of the refill (after the next step's reads)
+#pragma unroll
+        for (int o = ks * G::OPS / NKS; o < (ks + 1) * G::OPS / NKS; ++o) dma_op(o, nkt, nst);
       }
     }
     // instruction order for the scheduler: the first step's LDS reads, then
@@ -796,14 +801,19 @@ __global__ __launch_bounds__(G::NT) void gemm_nt_kernel(const T* __restrict__ A,
       }
       if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
       if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
+      // (spread: this step's share of the refill after its reads and products)
+      if constexpr (SPREAD) {
+        const int share = (ks + 1) * G::OPS / NKS - ks * G::OPS / NKS;
+        for (int o = 0; o < share; ++o) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
     }
     if constexpr (SPREAD) {
-      // the last step reads nothing, so its products carry the DMA issue
-      // (which, writing LDS, stays behind every fragment read before it)
+      // the last step reads nothing; its products carry its share of the DMA
+      constexpr int LAST = G::OPS - (NKS - 1) * G::OPS / NKS;
 #pragma unroll
       for (int r = 0; r < NM; ++r) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        constexpr int DQ = G::OPS / NM, DR = G::OPS % NM;   // DMA ops per product
+        constexpr int DQ = LAST / NM, DR = LAST % NM;   // DMA ops per product
         if (r < DR) __builtin_amdgcn_sched_group_barrier(0x020, DQ + 1, 0);
         else if constexpr (DQ > 0) __builtin_amdgcn_sched_group_barrier(0x020, DQ, 0);
       }
