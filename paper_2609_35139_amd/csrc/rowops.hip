@@ -5,6 +5,7 @@
 //  - the RoPE (cos, sin) table,
 //  - one-time weight preparation (transpose / widen).
 #include <algorithm>
+#include <cmath>
 #include <vector>
 
 #include "launch.h"
@@ -245,11 +246,13 @@ struct SchedBatch {
   unsigned first[SCHED_CHUNKS / 32];  // bit c: chunk c opens its request
 };
 
+constexpr int ROPE_MAX_HALF = 64;
 struct RopeRow {
   float2* tab;     // [token][half] (cos, sin), or null
   int half;        // d_head / 2 (1 without a table)
-  int d_head;
-  double theta;
+  // theta^(-2i / d_head) for i < half, in fp64 (formed on the host: one
+  // power per frequency instead of one per table entry)
+  double inv_freq[ROPE_MAX_HALF];
 };
 
 __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __restrict__ lo,
@@ -280,7 +283,7 @@ __global__ __launch_bounds__(256) void schedule_kernel(SchedBatch sb, int* __res
   }
   // (cos, sin)(p * theta^(-2i / d_head)), angle and cosines in fp64
   if (rr.tab) {
-    const double ang = (double)p * pow(rr.theta, -2.0 * (double)i / (double)rr.d_head);
+    const double ang = (double)p * rr.inv_freq[i];
     rr.tab[(int64_t)t * rr.half + i] = make_float2((float)cos(ang), (float)sin(ang));
   }
 }
@@ -289,8 +292,13 @@ hipError_t chunk_schedule(const int32_t* off, int32_t n_chunks, const int32_t* r
                           int32_t n_req, int mask, const int32_t* pos_offset, int* lo, int* hi,
                           int* pos, int* gpos, int* flags, hipStream_t s, float2* rope,
                           int d_head, double theta) {
-  RopeRow rr{rope, rope ? d_head / 2 : 1, d_head, theta};
-  if (rope && rr.half < 1) return hipErrorInvalidValue;
+  RopeRow rr{};
+  rr.tab = rope;
+  rr.half = rope ? d_head / 2 : 1;
+  if (rope && (rr.half < 1 || rr.half > ROPE_MAX_HALF)) return hipErrorInvalidValue;
+  if (rope)
+    for (int i = 0; i < rr.half; ++i)
+      rr.inv_freq[i] = std::pow(theta, -2.0 * (double)i / (double)d_head);
   std::vector<int> rs(n_chunks), re(n_chunks), gb(n_chunks), first(n_chunks);
   const int nr = req ? n_req : 1;
   for (int r = 0; r < nr; ++r) {
