@@ -81,6 +81,8 @@ template <typename T>
 struct EpiBias {
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
   static constexpr bool kWide = true;
+  // 64-column tiles are fine for bias epilogues (8-column segments)
+  static constexpr bool kNarrow = true;
   T* out; int64_t ldo; const float* bias; const T* resid; int64_t ldr; const T* resid2;
   int64_t ldr2; int gelu;
   template <int ROWS, int COLS, int NT>
@@ -152,6 +154,7 @@ struct EpiBias {
 template <typename T>
 struct EpiQKV {
   static constexpr bool kWide = false;   // head-aligned 128-column tiles
+  static constexpr bool kNarrow = false;
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias;
   const float2* rope;   // (cos, sin) per token
@@ -255,6 +258,7 @@ struct EpiQKV {
 template <typename T>
 struct EpiQKVh {
   static constexpr bool kWide = true;
+  static constexpr bool kNarrow = false;
   T* q; T* k; T* vt; int64_t n_pad; int d_b, d_head; const float* bias;
   const float2* rope;   // (cos, sin) per token
   __device__ int b_row(int n) const {
@@ -402,6 +406,7 @@ template <typename T>
 struct EpiExpand {
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
   static constexpr bool kWide = false;
+  static constexpr bool kNarrow = false;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
   // What the prefetch holds: the stale values of the thread's rows and a
@@ -495,6 +500,7 @@ template <typename T>
 struct EpiExpandRope {
   __device__ int b_row(int n) const { return n; }   // output column -> weight row
   static constexpr bool kWide = false;   // pair registers do not fit beside a 256x256 tile
+  static constexpr bool kNarrow = false;
   T* kv; KvStrides ks; const float* bias; const float* sigma; int mode; const int* keep;
   T* kvo; KvStrides kso;   // destination when repairing out of place (kvo null: in place)
   const float2* rope;      // [M][head_dim/2] scaled (cos, sin)
@@ -940,6 +946,15 @@ static hipError_t launch(const T* A, int64_t lda, const T* B, int64_t ldb, int M
                                                                     sp);
   }
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
+  // Grids of at most half the CUs (short batches) take 64x64 tiles instead:
+  // four times the workgroups (two resident per CU), each with a quarter of
+  // the operand bytes per slab, on eight waves as two 4-wave K groups of
+  // 32x32 waves.
+  if constexpr (sizeof(T) == 2 && Epi::kNarrow) {
+    if (tiles <= 128)
+      return launch_tiled<T, GemmTile<T, 1, 1, 4, 2, 2, false, 2>, Epi, SPLIT>(A, lda, B, ldb, M, N,
+                                                                              K, epi, s, sp);
+  }
   if (tiles <= 256) {
     // long K: two 4-wave groups of 64x64 waves, each on half of every slab's
     // k-steps, read a third fewer fragment bytes from LDS per product than
