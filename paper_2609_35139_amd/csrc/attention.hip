@@ -9,7 +9,8 @@
 // loaded) and applies per-element masking only on tiles that are not fully
 // inside every row's interval.
 //
-// A workgroup owns 128 queries of one head (32 per wave).  Scores are formed
+// A workgroup owns 128 queries of one head (32 per wave; 64 queries for
+// grids too small to fill the chip, see below).  Scores are formed
 // transposed, S^T = K Q^T, with 32x32 MFMA atoms, so that each lane holds the
 // scores of one query: the online-softmax max and sum are register
 // reductions plus one in-register exchange with lane ^ 32.  The K rows of
@@ -37,22 +38,29 @@ namespace cr {
 // largest tile row sum accepted without re-deriving the reference max
 constexpr float kMaxTileSum = 16777216.0f;   // 2^24
 
-template <typename T, int D, int STAGES_ = 4>
+// Eight waves per workgroup in GROUPS = 8 / WPG groups of WPG waves: a
+// workgroup owns BQ = 32 * WPG queries, and the groups split its key tiles.
+template <typename T, int D, int STAGES_ = 4, int WPG_ = 4>
 struct AttnCfg {
-  static constexpr int BQ = 128, BKV = 64, STAGES = STAGES_;
-  static constexpr int GROUPS = 2, NT = 256 * GROUPS;  // two 4-wave groups
+  static constexpr int WPG = WPG_, BQ = 32 * WPG, BKV = 64, STAGES = STAGES_;
+  static constexpr int GROUPS = 8 / WPG, NT = 512;
   static constexpr int VEC = 16 / (int)sizeof(T);
   static constexpr int RBK = D * (int)sizeof(T);      // K tile row bytes
   static constexpr int RBV = BKV * (int)sizeof(T);    // V^T tile row bytes
   static constexpr int K_BYTES = BKV * RBK, V_BYTES = D * RBV;
-  static constexpr int K_ROUNDS = K_BYTES / 4096, V_ROUNDS = V_BYTES / 4096;
+  // a group's waves fill 1 KB each per DMA round
+  static constexpr int K_ROUNDS = K_BYTES / (WPG * 1024), V_ROUNDS = V_BYTES / (WPG * 1024);
   static constexpr int OPS = K_ROUNDS + V_ROUNDS;     // DMA ops per thread per tile
   static constexpr int STAGE_BYTES = K_BYTES + V_BYTES;
   static constexpr int RING_BYTES = STAGES * STAGE_BYTES;
-  // merge area: group 1 hands (m, l, O^T) of its 128 queries to group 0;
-  // rows of D + 1 floats, so the 32 queries of a wave fall in distinct banks
+  // merge area: each group but the first hands (m, l, O^T) of its BQ
+  // queries to group 0; rows of D + 1 floats, so the 32 queries of a wave
+  // fall in distinct banks
   static constexpr int MLD = D + 1;
-  static constexpr int MERGE_BYTES = BQ * MLD * 4 + 2 * BQ * 2 * 4;
+  static constexpr int MERGE_ONE = BQ * MLD * 4 + 2 * BQ * 2 * 4;
+  static constexpr int MERGE_BYTES = (GROUPS - 1) * MERGE_ONE;
+  static_assert(GROUPS * WPG == 8 && K_ROUNDS * WPG * 1024 == K_BYTES &&
+                V_ROUNDS * WPG * 1024 == V_BYTES, "wave groups");
   static constexpr int LDS = GROUPS * RING_BYTES > MERGE_BYTES ? GROUPS * RING_BYTES : MERGE_BYTES;
 };
 
@@ -64,17 +72,20 @@ __device__ __forceinline__ int swap_bits23(int r) {
 __device__ __forceinline__ int score_key(int g, int i) { return (i >> 3) * 16 + g * 8 + (i & 7); }
 
 // Two groups of four waves share the 128 queries of a workgroup and split
-// its key tiles (group 0 even, group 1 odd tiles), each with its own online
+// its key tiles (group g takes tiles g, g + 2, ...), each with its own online
 // softmax state and LDS ring; group 1's partial result is merged into group
 // 0's at the end.  This halves the critical path of the long query tiles of
 // late chunks and keeps two waves per SIMD so that one wave's softmax
-// overlaps the other's MFMAs.
+// overlaps the other's MFMAs.  A grid of fewer workgroups than half the CUs
+// (a short batch) instead takes 64-query tiles with four groups of two
+// waves (tiles g, g + 4, ...; two-slot rings, merged in group order): twice
+// the workgroups, each group walking a quarter of the key tiles.
 //
 // Q arrives pre-scaled by log2(e)/sqrt(d_head) (QKV epilogue), so scores are
 // in exp2 units.  K and V^T are padded with finite rows up to n_pad, so tile
 // loads need no clamping.  The tile loop is unrolled over the STAGES ring
 // slots: every LDS address is a per-lane base plus a compile-time offset.
-template <typename T, int D, int STAGES = 4>
+template <typename T, int D, int STAGES = 4, int WPG = 4>
 __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
                                                         const T* __restrict__ Kg,
                                                         const T* __restrict__ Vt,
@@ -83,7 +94,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
                                                         const int* __restrict__ lo_arr,
                                                         const int* __restrict__ hi_arr,
                                                         int n_qtiles) {
-  using C = AttnCfg<T, D, STAGES>;
+  using C = AttnCfg<T, D, STAGES, WPG>;
   using MM = Mma32<T>;
   using frag = typename MM::frag;
   using SK = Swz<C::RBK>;
@@ -96,7 +107,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2, gw = wave & 3;
+  const int grp = wave / WPG, gw = wave % WPG;
   const int g = lane >> 5, ql = lane & 31;
   const int head = blockIdx.x % n_heads;
   const int qt = n_qtiles - 1 - blockIdx.x / n_heads;   // latest (longest) tiles first
@@ -117,8 +128,8 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   const int mlo = qvalid ? lo_arr[q] : INT_MIN, mhi = qvalid ? hi_arr[q] : INT_MAX;
   const int kb = (kv_begin / C::BKV) * C::BKV;
   const int ntiles = (kv_end - kb + C::BKV - 1) / C::BKV;
-  const int iters = (ntiles + 1) / 2;                  // tiles per group (group 1 may idle last)
-  const int mine = (ntiles - grp + 1) / 2;             // tiles this group owns
+  const int iters = (ntiles + C::GROUPS - 1) / C::GROUPS;          // tiles per group
+  const int mine = (ntiles - grp + C::GROUPS - 1) / C::GROUPS;     // tiles this group owns
 
   // Q^T fragments stay in registers: col = query, k = d
   frag qf[QF];
@@ -134,13 +145,13 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   const char* vsrc[C::V_ROUNDS];
 #pragma unroll
   for (int r = 0; r < C::K_ROUNDS; ++r) {
-    const int row = (r * 4 + gw) * SK::RPW + lane / SK::CPR;
+    const int row = (r * WPG + gw) * SK::RPW + lane / SK::CPR;
     const int chunk = SK::slot(row, lane % SK::CPR);
     ksrc[r] = reinterpret_cast<const char*>(Kg + (int64_t)(kb + row) * d_b + head * D) + chunk * 16;
   }
 #pragma unroll
   for (int r = 0; r < C::V_ROUNDS; ++r) {
-    const int row = (r * 4 + gw) * SV::RPW + lane / SV::CPR;
+    const int row = (r * WPG + gw) * SV::RPW + lane / SV::CPR;
     const int chunk = SV::slot(row, lane % SV::CPR);
     vsrc[r] = reinterpret_cast<const char*>(Vt + ((int64_t)head * D + row) * n_pad + kb) + chunk * 16;
   }
@@ -179,13 +190,13 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
   // group-local tile i (workgroup tile 2i + grp) into ring slot SLOT
   auto issue = [&](int i, int slot_bytes) {
     char* base = ring + slot_bytes;
-    const int64_t tile = 2 * i + grp;
+    const int64_t tile = (int64_t)C::GROUPS * i + grp;
 #pragma unroll
     for (int r = 0; r < C::K_ROUNDS; ++r)
-      dma16(ksrc[r] + tile * ktile_bytes, base + (r * 4 + gw) * 1024);
+      dma16(ksrc[r] + tile * ktile_bytes, base + (r * WPG + gw) * 1024);
 #pragma unroll
     for (int r = 0; r < C::V_ROUNDS; ++r)
-      dma16(vsrc[r] + tile * C::BKV * (int64_t)sizeof(T), base + C::K_BYTES + (r * 4 + gw) * 1024);
+      dma16(vsrc[r] + tile * C::BKV * (int64_t)sizeof(T), base + C::K_BYTES + (r * WPG + gw) * 1024);
   };
 
   // one key tile held in ring slot J (compile time)
@@ -197,7 +208,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     // STAGES-2 later ones remain in flight
     wait_vmcnt<(C::STAGES - 2) * C::OPS>();
     __builtin_amdgcn_s_barrier();   // the slot refilled below is no longer read by anyone
-    if (it >= mine) return;         // group 1 without a last tile: only keeps the barrier count
+    if (it >= mine) return;         // a group without a tile this round: only keeps the barrier count
     constexpr int SO = J * C::STAGE_BYTES;
     // the compiler's interleaving of LDS reads with MFMAs for this tile's
     // fragment reads and score products (-2% per launch, same results)
@@ -238,7 +249,7 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
 #pragma unroll
       for (int kk = 1; kk < QF; ++kk) s[rt] = MM::mma(kf[rt][kk], qf[kk], s[rt]);
     }
-    const int k0 = kb + (2 * it + grp) * C::BKV;
+    const int k0 = kb + (C::GROUPS * it + grp) * C::BKV;
     if (!(k0 >= wmax_lo && k0 + C::BKV <= wmin_hi)) {
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
@@ -327,14 +338,17 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     if constexpr (C::STAGES > 3) step(std::integral_constant<int, 3 % C::STAGES>{}, it0 + 3);
   }
 
-  // merge group 1 into group 0: per query q' = gw*32 + ql, lane half g holds
-  // l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4 of O^T
+  // merge the other groups into group 0: per query q' = gw*32 + ql, lane half
+  // g holds l (partial over its keys) and rows d = dt*32 + (v/4)*8 + g*4 + v%4
+  // of O^T; group gi > 0 hands them over in merge region gi - 1
   wait_vmcnt<0>();   // the copies past the last tile land in the rings
-  __syncthreads();   // both rings idle
-  float* mo = reinterpret_cast<float*>(lds);                  // [BQ][MLD] O^T values
-  float* ml = mo + C::BQ * C::MLD;                            // [BQ][2] (m, l) per lane half
+  __syncthreads();   // every ring idle
+  auto mo_of = [&](int gi) { return reinterpret_cast<float*>(lds + (gi - 1) * C::MERGE_ONE); };
+  auto ml_of = [&](int gi) { return mo_of(gi) + C::BQ * C::MLD; };   // [BQ][2] (m, l) per half
   const int qrow = gw * 32 + ql;
-  if (grp == 1) {
+  if (grp >= 1) {
+    float* mo = mo_of(grp);
+    float* ml = ml_of(grp);
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
@@ -344,30 +358,75 @@ __global__ __launch_bounds__(512) void attention_kernel(const T* __restrict__ Q,
     ml[(qrow * 2 + g) * 2 + 1] = lsum;
   }
   __syncthreads();
-  if (grp == 1 || !qvalid) return;
-  const float m1 = ml[(qrow * 2 + g) * 2 + 0], l1 = ml[(qrow * 2 + g) * 2 + 1];
-  const float mt = fmaxf(m_ref, m1);
-  const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mt);
-  const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mt);
-  const float lpart = lsum * a0 + l1 * a1;
-  const float total = halves_sum(lpart);
-  const float inv = 1.0f / total;
+  if (grp >= 1 || !qvalid) return;
   T* orow = O + (int64_t)q * d_b + head * D;
+  auto store4 = [&](int dd, const float* vals) {
+    T outv[4];
 #pragma unroll
-  for (int d = 0; d < DT; ++d)
-#pragma unroll
-    for (int i4 = 0; i4 < 4; ++i4) {
-      const int dd = d * 32 + i4 * 8 + g * 4;
-      T outv[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        outv[e] = from_f32<T>((oacc[d][i4 * 4 + e] * a0 + mo[qrow * C::MLD + dd + e] * a1) * inv);
-      if constexpr (sizeof(T) == 2) {
-        *reinterpret_cast<uint2*>(orow + dd) = *reinterpret_cast<const uint2*>(outv);
-      } else {
-        *reinterpret_cast<uint4*>(orow + dd) = *reinterpret_cast<const uint4*>(outv);
-      }
+    for (int e = 0; e < 4; ++e) outv[e] = from_f32<T>(vals[e]);
+    if constexpr (sizeof(T) == 2) {
+      *reinterpret_cast<uint2*>(orow + dd) = *reinterpret_cast<const uint2*>(outv);
+    } else {
+      *reinterpret_cast<uint4*>(orow + dd) = *reinterpret_cast<const uint4*>(outv);
     }
+  };
+  if constexpr (C::GROUPS == 2) {
+    const float* mo = mo_of(1);
+    const float* ml = ml_of(1);
+    const float m1 = ml[(qrow * 2 + g) * 2 + 0], l1 = ml[(qrow * 2 + g) * 2 + 1];
+    const float mt = fmaxf(m_ref, m1);
+    const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mt);
+    const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mt);
+    const float lpart = lsum * a0 + l1 * a1;
+    const float total = halves_sum(lpart);
+    const float inv = 1.0f / total;
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int dd = d * 32 + i4 * 8 + g * 4;
+        float vals[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          vals[e] = (oacc[d][i4 * 4 + e] * a0 + mo[qrow * C::MLD + dd + e] * a1) * inv;
+        store4(dd, vals);
+      }
+  } else {
+    // groups combined in index order with one common max
+    float mg[C::GROUPS], lg[C::GROUPS], ag[C::GROUPS];
+    mg[0] = m_ref;
+    lg[0] = lsum;
+#pragma unroll
+    for (int gi = 1; gi < C::GROUPS; ++gi) {
+      mg[gi] = ml_of(gi)[(qrow * 2 + g) * 2 + 0];
+      lg[gi] = ml_of(gi)[(qrow * 2 + g) * 2 + 1];
+    }
+    float mt = mg[0];
+#pragma unroll
+    for (int gi = 1; gi < C::GROUPS; ++gi) mt = fmaxf(mt, mg[gi]);
+    float lpart = 0.f;
+#pragma unroll
+    for (int gi = 0; gi < C::GROUPS; ++gi) {
+      ag[gi] = mg[gi] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mg[gi] - mt);
+      lpart += lg[gi] * ag[gi];
+    }
+    const float inv = 1.0f / halves_sum(lpart);
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int dd = d * 32 + i4 * 8 + g * 4;
+        float vals[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float o = oacc[d][i4 * 4 + e] * ag[0];
+#pragma unroll
+          for (int gi = 1; gi < C::GROUPS; ++gi) o += mo_of(gi)[qrow * C::MLD + dd + e] * ag[gi];
+          vals[e] = o * inv;
+        }
+        store4(dd, vals);
+      }
+  }
 }
 
 template <typename T>
@@ -379,6 +438,25 @@ hipError_t attention(const T* q, const T* k, const T* vt, T* o, int N, int d_b, 
   dim3 grid(n_qtiles * n_heads);
   // two rings (one per wave group) must fit in 160 KB of LDS
   constexpr int kStages = sizeof(T) == 2 ? 4 : 2;
+  // A grid of fewer workgroups than half the CUs (short batches) takes
+  // 64-query tiles whose four 2-wave groups split the key tiles (two-slot
+  // rings): twice the workgroups, each with half the key tiles per group.
+  if constexpr (sizeof(T) == 2) {
+    if ((int64_t)n_qtiles * n_heads < 128) {
+      const int n_q64 = (N + 63) / 64;
+      dim3 g64(n_q64 * n_heads);
+      if (d_head == 64) {
+        CR_LAUNCH((attention_kernel<T, 64, 2, 2>), g64, dim3(512), 0, s, q, k, vt, o, N, d_b,
+                  n_heads, n_pad, lo, hi, n_q64);
+        return hipGetLastError();
+      }
+      if (d_head == 32) {
+        CR_LAUNCH((attention_kernel<T, 32, 2, 2>), g64, dim3(512), 0, s, q, k, vt, o, N, d_b,
+                  n_heads, n_pad, lo, hi, n_q64);
+        return hipGetLastError();
+      }
+    }
+  }
   if (d_head == 64) {
     CR_LAUNCH((attention_kernel<T, 64, kStages>), grid, dim3(512), 0, s, q, k, vt, o, N, d_b,
               n_heads, n_pad, lo, hi, n_qtiles);
