@@ -80,6 +80,14 @@ SMALL = [
          d_b=128, n_heads=2, d_seg=8, n_blocks=0),
     dict(lengths=((40, 97),), dtype="f32", L=2, H=1, dh=64, E=64, d_c=64, d_b=128,
          n_heads=4, d_seg=8, n_blocks=0),
+    # 1,177 ragged tokens with 16 and 32 heads: at least 128 query tiles x
+    # heads, so the attention takes its 128-query tiles (64- and 32-wide
+    # heads, last tile ragged) while the 1,024-column GEMMs still take the
+    # 64x64 tiles of short batches and FFN1 the 128-row ones
+    dict(lengths=((300, 1, 517), (260, 99)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
+         d_b=1024, n_heads=16, d_seg=8),
+    dict(lengths=((300, 1, 517), (260, 99)), dtype="bf16", L=1, H=2, dh=64, E=128, d_c=64,
+         d_b=1024, n_heads=32, d_seg=8),
     # one token per chunk (block-causal = token-causal): every key tile masked
     dict(lengths=((1,) * 150, (1,) * 20), dtype="bf16", L=1, H=2, dh=64, E=64, d_c=64,
          d_b=128, n_heads=2, d_seg=8),
