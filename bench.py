@@ -227,7 +227,7 @@ def main():
                          "flushed (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs the repair of one request batch on one GPU; "
+        print(f"bench.py: the library runs the repair of one request batch on one GPU; "
               f"--gpus {args.gpus} is not supported (multi-GPU sharding is design-only).",
               file=sys.stderr)
         sys.exit(2)

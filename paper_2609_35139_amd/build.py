@@ -76,7 +76,7 @@ def build(verbose: bool = False) -> str:
             rest = "\n".join(l for l in out.splitlines() if "kernel-resource-usage" not in l)
             if verbose and rest.strip():
                 print(rest)
-    # per-kernel register and scratch use of this build (a spill to scratch
+    # per-kernel register and scratch use of the compiled kernels (a spill to scratch
     # memory in a hot kernel is a performance bug the tests look for)
     with open(RESOURCES, "w") as fh:
         for r in rows:
