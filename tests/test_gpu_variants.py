@@ -226,3 +226,28 @@ def test_global_placement_at_the_4x256_workload():
     Yr = oracle_repair(inp, global_rope=dict(inv_freq=_freqs(t.head_dim, 1e6), scale=1.0,
                                              position_offset=[37]))
     assert_parity(Y, Yr, X, w)
+
+
+# 1,177 ragged tokens in 16 heads of 64: at least 128 query tiles x heads, so
+# the attention takes its 128-query tiles (the small cases above and the
+# 4 x 256 workload take the 64-query tiles of short batches)
+WIDE = dict(lengths=((300, 1, 517), (260, 99)), dtype="bf16", L=2, H=2, dh=64, E=128, d_c=64,
+            d_b=1024, n_heads=16, d_seg=8)
+
+
+@pytest.mark.parametrize("name", ["token_causal", "bidirectional", "block_diagonal"])
+def test_topologies_on_128_query_tiles(name):
+    from paper_2609_35139_amd.binding import Options
+    w, inp, X = _case(WIDE)
+    Y = gpu_repair(inp, options=Options(mask=name))
+    assert_parity(Y, oracle_repair(inp, mask=name), X, w)
+
+
+def test_global_placement_on_128_query_tiles():
+    from paper_2609_35139_amd.binding import Options
+    w, inp, X = _case(WIDE)
+    t = w.target
+    Y = gpu_repair(inp, options=Options(global_rope=dict(theta=1e4), position_offset=[5, 900]))
+    Yr = oracle_repair(inp, global_rope=dict(inv_freq=_freqs(t.head_dim, 1e4), scale=1.0,
+                                             position_offset=[5, 900]))
+    assert_parity(Y, Yr, X, w)
