@@ -101,7 +101,10 @@ def kernel_stats(stats_csv, bench_json, command):
                 "#   " + ", ".join("%s %.2f (%d)" % (c, sum(v) / len(v), len(v))
                                    for c, v in durs.items())]
     rf = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in b["roofline"].items()}
-    out += ["", "# bench line of the same command (live HIP events on the library's stream):",
+    out += ["", "# bench line of the same command (live HIP events on the library's stream;",
+            "# under the tracer each interval also holds the tracer's own handling of",
+            "# the dispatch, a few us per launch, so short kernels read long here and",
+            "# the reported bench line is the one of an untraced run):",
             "#   ms_per_step %.3f, value %.4g tokens/s" % (b["ms_per_step"], b["value"]),
             "#   roofline " + json.dumps(rf),
             "#   per-class average launch (us): " +
